@@ -1,0 +1,174 @@
+"""Seeded synthetic workloads for sharded layerwise QK-Norm.
+
+This module only draws inputs: projected Q and K activations (as bf16 bit
+patterns), the fp32 gamma vectors, and the shard layout. It holds none of the
+normalisation arithmetic, so both the fp64 oracle and the HIP path can take
+their inputs from here without sharing any of the method's code.
+
+Shapes follow the tensor-parallel layout of the paper (Sec. II-B, Fig. 1(b)):
+the column-parallel Q/K projection leaves rank r with a contiguous slice of
+the hidden dimension of Q and of K. The paper's own workloads (OLMoE, OLMo 2,
+OLMo 3 serving ShareGPT prompts, Sec. IV-A) need weights and a dataset that
+are not available; the named workloads below stand in for them with GQA-style
+Q/K widths and decode/prefill token counts.
+
+Recipe (shared by every workload):
+  * one ``numpy.random.Generator`` per stream, seeded with
+    ``SeedSequence([seed, stream_id])``; stream ids: 0 = X_Q, 1 = X_K,
+    2 = per-token scales, 3 = outlier channels, 4 = gamma_Q, 5 = gamma_K;
+  * activations are drawn in fp32, shaped by the workload's distribution,
+    then rounded to bf16 with round-to-nearest-even; everyone consumes the
+    same bf16 bits;
+  * lognormal(mu, sigma) = exp(N(mu, sigma)), one draw per token per tensor,
+    multiplying that token's whole (unsharded) row;
+  * outlier channels: n = max(1, round(0.001 * d_full)) channels per tensor,
+    picked without replacement, fixed across tokens, scaled x50 before the
+    bf16 rounding;
+  * Student-t uses ``Generator.standard_t(df)``;
+  * gamma ~ U[0.5, 1.5), stored as fp32.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+from typing import Dict, Tuple
+
+import numpy as np
+
+STREAM_XQ, STREAM_XK, STREAM_SCALE, STREAM_OUTLIER, STREAM_GQ, STREAM_GK = range(6)
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One QK-Norm workload: T tokens, full Q/K widths, TP degree, distribution."""
+
+    name: str
+    T: int
+    q_full: int
+    k_full: int
+    tp: int
+    dist: str  # "normal" | "normal_lognormal" | "normal_outliers" | "student_t"
+    seed: int
+    sigma: float = 0.0  # lognormal sigma for "normal_lognormal"
+    df: float = 3.0  # degrees of freedom for "student_t"
+    eps: float = 1e-6
+
+    @property
+    def q_local(self) -> int:
+        return self.q_full // self.tp
+
+    @property
+    def k_local(self) -> int:
+        return self.k_full // self.tp
+
+    def with_tp(self, tp: int) -> "Workload":
+        """Same tokens and data, another TP degree (the data do not depend on tp)."""
+        if self.q_full % tp or self.k_full % tp:
+            raise ValueError(f"tp={tp} does not divide {self.q_full}/{self.k_full}")
+        return replace(self, tp=tp, name=f"{self.name}@tp{tp}")
+
+    def with_tokens(self, T: int) -> "Workload":
+        return replace(self, T=T, name=f"{self.name}@T{T}")
+
+
+# The five workloads. Seeds: the tiny case uses seed 0; the others 1..4.
+TINY_FULL = Workload("tiny_full_T16_q512_k128_tp1", 16, 512, 128, 1, "normal", 0)
+DECODE_TP4 = Workload("decode_T64_q4096_k1024_tp4", 64, 4096, 1024, 4,
+                      "normal_lognormal", 1, sigma=1.0)
+DECODE_TP8 = Workload("decode_T256_q5120_k1024_tp8", 256, 5120, 1024, 8,
+                      "normal_outliers", 2)
+PREFILL_TP2 = Workload("prefill_T8192_q4096_k1024_tp2", 8192, 4096, 1024, 2,
+                       "normal_lognormal", 3, sigma=0.5)
+LONG_PREFILL_TP4 = Workload("long_prefill_T32768_q8192_k1024_tp4", 32768, 8192, 1024, 4,
+                            "student_t", 4, df=3.0)
+
+WORKLOADS: Dict[str, Workload] = {w.name: w for w in
+                                  (TINY_FULL, DECODE_TP4, DECODE_TP8, PREFILL_TP2, LONG_PREFILL_TP4)}
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (round to nearest, ties to even); return uint16 bits.
+
+    Input conversion only (the data format), not part of the normalisation.
+    NaN inputs map to a quiet NaN of the same sign.
+    """
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    rounded = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    nan = np.isnan(a)
+    if nan.any():
+        rounded[nan] = ((u[nan] >> 16).astype(np.uint16) & 0x8000) | 0x7FC0
+    return rounded
+
+
+def _rng(seed: int, stream: int) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([seed, stream]))
+
+
+def _activations(wl: Workload, d_full: int, stream: int, scale_col: int) -> np.ndarray:
+    rng = _rng(wl.seed, stream)
+    T = wl.T
+    if wl.dist == "student_t":
+        x = rng.standard_t(wl.df, size=(T, d_full)).astype(np.float32)
+    else:
+        x = rng.standard_normal(size=(T, d_full), dtype=np.float32)
+    if wl.dist == "normal_lognormal":
+        # one scale per token per tensor; column 0 = Q, column 1 = K
+        s = np.exp(_rng(wl.seed, STREAM_SCALE).normal(0.0, wl.sigma, size=(T, 2)))
+        x *= s[:, scale_col:scale_col + 1].astype(np.float32)
+    elif wl.dist == "normal_outliers":
+        idx = outlier_channels(wl)[scale_col]
+        x[:, idx] *= np.float32(50.0)
+    elif wl.dist not in ("normal", "student_t"):
+        raise ValueError(f"unknown distribution {wl.dist!r}")
+    return x
+
+
+def outlier_channels(wl: Workload) -> Tuple[np.ndarray, np.ndarray]:
+    """The outlier channel indices of a "normal_outliers" workload (Q, K).
+
+    Q's channels are drawn first, then K's, from one stream.
+    """
+    orng = _rng(wl.seed, STREAM_OUTLIER)
+    nq = max(1, round(0.001 * wl.q_full))
+    nk = max(1, round(0.001 * wl.k_full))
+    return (orng.choice(wl.q_full, size=nq, replace=False),
+            orng.choice(wl.k_full, size=nk, replace=False))
+
+
+def generate(wl: Workload) -> Dict[str, np.ndarray]:
+    """Full (unsharded) inputs of a workload.
+
+    Returns ``xq`` uint16 [T, q_full], ``xk`` uint16 [T, k_full] (bf16 bits),
+    ``gq`` float32 [q_full], ``gk`` float32 [k_full].
+    """
+    xq = f32_to_bf16_bits(_activations(wl, wl.q_full, STREAM_XQ, 0))
+    xk = f32_to_bf16_bits(_activations(wl, wl.k_full, STREAM_XK, 1))
+    gq = _rng(wl.seed, STREAM_GQ).uniform(0.5, 1.5, size=wl.q_full).astype(np.float32)
+    gk = _rng(wl.seed, STREAM_GK).uniform(0.5, 1.5, size=wl.k_full).astype(np.float32)
+    return {"xq": xq, "xk": xk, "gq": gq, "gk": gk}
+
+
+def shard_cols(d_full: int, tp: int, rank: int) -> slice:
+    """Columns held by `rank`: a contiguous slice, as column-parallel projections leave them."""
+    if d_full % tp:
+        raise ValueError(f"tp={tp} does not divide d_full={d_full}")
+    d_local = d_full // tp
+    return slice(rank * d_local, (rank + 1) * d_local)
+
+
+def random_rows(seed: int, T: int, d: int, dist: str = "normal", scale: float = 1.0) -> np.ndarray:
+    """Small ad-hoc bf16 inputs for edge-case tests (uint16 bits, [T, d])."""
+    rng = _rng(seed, 100)
+    if dist == "normal":
+        x = rng.standard_normal(size=(T, d), dtype=np.float32)
+    elif dist == "student_t":
+        x = rng.standard_t(3.0, size=(T, d)).astype(np.float32)
+    elif dist == "uniform":
+        x = rng.uniform(-1.0, 1.0, size=(T, d)).astype(np.float32)
+    else:
+        raise ValueError(dist)
+    return f32_to_bf16_bits(x * np.float32(scale))
+
+
+def random_gamma(seed: int, d: int) -> np.ndarray:
+    return _rng(seed, 101).uniform(0.5, 1.5, size=d).astype(np.float32)
