@@ -1,0 +1,175 @@
+/*
+ * qkn.h -- C ABI of libqkn: sharded layerwise QK-Norm on AMD MI355X (gfx950).
+ *
+ * Layerwise QK-Norm applies RMSNorm (Eq. 1, Sec. II-A of SwiftQK,
+ * arXiv 2608.09160) to each token's full projected Q vector and, separately,
+ * to its full projected K vector:
+ *
+ *     y = x / sqrt( (1/H) * sum_j x_j^2 + eps ) * gamma,     H = full width.
+ *
+ * Under tensor parallelism (Sec. II-B) rank r of tp holds a contiguous slice of
+ * the hidden dimension. The method (Sec. III, Alg. 1) splits the norm into
+ *   Phase A  the rank's partial sum of squares of its slice, in fp32;
+ *   Phase B  the sum of all ranks' partials in ascending rank order, the factor
+ *            1/sqrt(S/H_total + eps), and -- independent of it -- x * gamma;
+ *   Phase C  the scaled shard, the only output written.
+ * This library computes one rank's share on one GPU. The other ranks' partials
+ * are inputs: device memory that the caller filled (in a real deployment they
+ * would arrive over the interconnect).
+ *
+ * Conventions for every entry point
+ *   - bf16 tensors are passed as uint16_t bit patterns; fp32 as float.
+ *   - Every pointer is DEVICE memory, owned by the caller. The library never
+ *     allocates or frees device memory and keeps no pointer after returning.
+ *   - A row-major tensor [T, ld] uses columns [0, d_local) of each row;
+ *     ld is in elements and must be >= d_local.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *     Calls are asynchronous on that stream and never synchronise the host.
+ *   - Arguments are validated before any HIP call, so an invalid call fails
+ *     without touching the GPU. T == 0 is a valid no-op (nothing launched).
+ *   - Errors are returned as negative status codes; nothing aborts and no C++
+ *     exception crosses the ABI. Faults during kernel execution surface, as
+ *     usual for HIP, at the caller's next synchronisation.
+ *   - Arithmetic: bf16 inputs are widened exactly, all sums and products are
+ *     fp32, the output is rounded once to bf16 (nearest, ties to even).
+ *     NaN and infinities propagate by IEEE rules (eps = 0 with an all-zero row
+ *     gives NaN).
+ *   - Determinism: a row's partial sum depends only on d_local and the row's
+ *     values (one fixed fp32 summation tree), never on the launch shape or the
+ *     entry point, so every rank combines bit-identical statistics.
+ *   - Fast path: 128-bit accesses when x, y are 16-byte aligned, w is 16-byte
+ *     aligned, and ld and d_local are multiples of 8, with d_local <= 4096 and
+ *     tp <= 64; otherwise a general path gives the same bits, more slowly.
+ *     Alignment is never an error.
+ */
+#ifndef QKN_H
+#define QKN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define QKN_OK 0
+#define QKN_EINVAL (-1)   /* bad argument: NULL required pointer, bad size, tp/rank, eps */
+#define QKN_EOVERLAP (-2) /* an output overlaps an input or another output in part */
+#define QKN_EHIP (-3)     /* the HIP runtime refused a query or a launch */
+
+/*
+ * One tensor (Q or K) of one rank.
+ *   x        bf16 [T, ldx], the rank's slice; columns [0, d_local) are used.
+ *   w        fp32 [d_local], the rank's slice of gamma.
+ *   partials fp32 [tp * T], rank-major: element k*T + t is rank k's partial
+ *            sum of squares of token t (the per-rank statistic exchanged in
+ *            Sec. III-A; a buffer slot per rank and token as in Alg. 1).
+ *            The fused call writes slot `rank` and reads every other slot.
+ *   y        bf16 [T, ldy] output; y == x with ldy == ldx runs in place
+ *            (Alg. 1 overwrites the local input); any other overlap with an
+ *            input is QKN_EOVERLAP.
+ *   inv_rms  optional fp32 [T]: receives 1/sqrt(S/d_full + eps). NULL skips.
+ *   d_local  width of the slice (>= 1).
+ *   d_full   width of the full vector, H_total of Alg. 1: the divisor of the
+ *            mean (>= d_local).
+ */
+typedef struct qkn_seg {
+  const uint16_t* x;
+  int64_t ldx;
+  const float* w;
+  float* partials;
+  uint16_t* y;
+  int64_t ldy;
+  float* inv_rms;
+  int64_t d_local;
+  int64_t d_full;
+} qkn_seg;
+
+/*
+ * Phase A alone (Sec. III-A; Alg. 1, Phase A):
+ *   partial_out[t] = sum_{j < d_local} x[t, j]^2   (fp32, fixed tree).
+ * x bf16 [T, ldx]; partial_out fp32 [T]. The result is bit-identical to the
+ * statistic the fused call computes for the same slice, so it serves as a
+ * peer rank's contribution. QKN_EINVAL: x or partial_out NULL with T > 0,
+ * T < 0, d_local < 1, ldx < d_local. QKN_EOVERLAP: partial_out overlaps x.
+ */
+int qkn_partial_sumsq(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                      float* partial_out, void* stream);
+
+/*
+ * Phases B and C from precomputed statistics (the unfused second step of a
+ * scalar-aggregation norm, Sec. IV-A):
+ *   S[t] = sum_{k=0}^{tp-1} partials[k*T + t]   (ascending k, fp32),
+ *   y[t, j] = bf16( (x[t, j] * w[j]) * (1 / sqrt(S[t]/d_full + eps)) ).
+ * partials fp32 [tp * T] holds every rank's slot, this rank's included.
+ * inv_rms may be NULL. QKN_EINVAL: NULL x/w/partials/y with T > 0, T < 0,
+ * tp < 1, d_local < 1, d_full < d_local, ldx or ldy < d_local, eps < 0 or not
+ * finite. QKN_EOVERLAP: y overlaps x in part, or a float output overlaps a
+ * bf16 tensor or the other float arrays.
+ */
+int qkn_apply(const uint16_t* x, int64_t ldx, const float* w, const float* partials,
+              int tp, int64_t T, int64_t d_local, int64_t d_full, float eps,
+              uint16_t* y, int64_t ldy, float* inv_rms, void* stream);
+
+/*
+ * The fused sharded QK-Norm of one rank (Sec. III, Alg. 1), Phases A+B+C in
+ * one persistent launch for 1 or 2 tensors (Q and K of the same tokens):
+ * each resident wavefront loops over tokens; per token and tensor it computes
+ * the slice's partial sum of squares, writes it to partials[rank*T + t] (if
+ * partials is not NULL), combines it with the other ranks' slots in ascending
+ * rank order, forms x * w while those slots are in flight, and writes the
+ * scaled slice. With tp == 1 no slot is read and partials may be NULL.
+ * QKN_EINVAL: segs NULL, nseg not 1 or 2, tp < 1, rank not in [0, tp), T < 0,
+ * eps < 0 or not finite, or a segment with a NULL x/w/y, partials NULL while
+ * tp > 1, d_local < 1, d_full < d_local, ldx or ldy < d_local.
+ * QKN_EOVERLAP: as for qkn_apply, across both segments.
+ */
+int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
+                    void* stream);
+
+/*
+ * Full-vector QK-Norm at TP = 1 (Eq. 1 on whole rows), the compute half of
+ * the all-gather baseline (Sec. II-C, Sec. IV-A). Same as qkn_fused_shard
+ * with tp = 1, rank = 0; each segment must have d_local == d_full; partials
+ * may be NULL (else it receives the full sum of squares per token).
+ */
+int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream);
+
+/* Static text for a status code (never NULL). */
+const char* qkn_strerror(int status);
+
+/*
+ * Launch description of the calling thread's most recent successful launch,
+ * for tests and benchmarks. kernel is a static string naming the variant
+ * ("rows<4,1>/fused", "generic/apply", ...); grid is in workgroups, block in
+ * threads, waves = grid * block / 64, lds_bytes is the dynamic LDS per
+ * workgroup.
+ */
+typedef struct qkn_launch_info {
+  const char* kernel;
+  int64_t grid;
+  int64_t block;
+  int64_t waves;
+  int64_t lds_bytes;
+} qkn_launch_info;
+int qkn_last_launch(qkn_launch_info* info);
+
+/*
+ * Process-wide tuning knobs (for benchmarks and tests; not thread-safe with
+ * concurrent launches). Keys:
+ *   "waves_per_cu"   cap on resident wavefronts per CU used to size the
+ *                    persistent grid (0 = occupancy limit, the default);
+ *   "waves_per_block" 1..4, 0 = automatic;
+ *   "force_generic"  1 = always take the general path (same results);
+ *   "validate_only"  1 = entry points validate their arguments and choose a
+ *                    kernel (reported by qkn_last_launch, grid 0) but make no
+ *                    HIP call and launch nothing.
+ * Returns QKN_OK or QKN_EINVAL for an unknown key or a bad value.
+ */
+int qkn_set_option(const char* key, int64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QKN_H */

@@ -1,0 +1,206 @@
+"""ctypes binding of libqkn (include/qkn.h): argument marshalling only.
+
+Every step of the computation runs in the HIP kernels of libqkn.so. This
+module checks tensor dtypes, devices and shapes, turns tensors into device
+pointers and strides, passes torch's current HIP stream, and maps status codes
+to exceptions. There is no fallback: if the library is missing, loading fails
+loudly (build it with ``python -m paper_2608_09160_amd.build``).
+
+Tensors: bf16 activations are ``torch.bfloat16`` 2-D tensors whose last
+dimension is contiguous (any row stride, so column slices of a wider buffer
+work); gamma, partials and inv_rms are ``torch.float32``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqkn.so")
+
+QKN_OK, QKN_EINVAL, QKN_EOVERLAP, QKN_EHIP = 0, -1, -2, -3
+
+_c_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+
+
+class QknSeg(ctypes.Structure):
+    _fields_ = [("x", _vp), ("ldx", _c_i64), ("w", _vp), ("partials", _vp),
+                ("y", _vp), ("ldy", _c_i64), ("inv_rms", _vp),
+                ("d_local", _c_i64), ("d_full", _c_i64)]
+
+
+class QknLaunchInfo(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_char_p), ("grid", _c_i64), ("block", _c_i64),
+                ("waves", _c_i64), ("lds_bytes", _c_i64)]
+
+
+class QknError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {qkn_strerror(status)} (status {status})")
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libqkn.so once and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libqkn.so not found at {path}; build it with "
+                           "`python -m paper_2608_09160_amd.build`")
+    lib = ctypes.CDLL(path)
+    lib.qkn_partial_sumsq.argtypes = [_vp, _c_i64, _c_i64, _c_i64, _vp, _vp]
+    lib.qkn_apply.argtypes = [_vp, _c_i64, _vp, _vp, ctypes.c_int, _c_i64, _c_i64, _c_i64,
+                              ctypes.c_float, _vp, _c_i64, _vp, _vp]
+    lib.qkn_fused_shard.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_int, _c_i64, ctypes.c_float, _vp]
+    lib.qkn_full.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, _c_i64, ctypes.c_float, _vp]
+    lib.qkn_strerror.argtypes = [ctypes.c_int]
+    lib.qkn_strerror.restype = ctypes.c_char_p
+    lib.qkn_last_launch.argtypes = [ctypes.POINTER(QknLaunchInfo)]
+    lib.qkn_set_option.argtypes = [ctypes.c_char_p, _c_i64]
+    for name in ("qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
+                 "qkn_last_launch", "qkn_set_option"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str) -> None:
+    if status != QKN_OK:
+        raise QknError(status, where)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _rows(t: torch.Tensor, what: str):
+    """(pointer, leading dimension, T, width) of a bf16 [T, width] tensor."""
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{what}: expected torch.bfloat16, got {t.dtype}")
+    if t.dim() != 2:
+        raise ValueError(f"{what}: expected a 2-D [T, d] tensor, got shape {tuple(t.shape)}")
+    if t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError(f"{what}: the last dimension must be contiguous")
+    if not t.is_cuda:
+        raise ValueError(f"{what}: must be a GPU tensor")
+    ld = t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+    return t.data_ptr(), ld, t.shape[0], t.shape[1]
+
+
+def _f32(t: Optional[torch.Tensor], what: str, numel: Optional[int] = None) -> Optional[int]:
+    if t is None:
+        return None
+    if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{what}: expected a contiguous float32 GPU tensor")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{what}: needs {numel} elements, has {t.numel()}")
+    return t.data_ptr()
+
+
+# --------------------------------------------------------------------- entry points
+
+def qkn_strerror(status: int) -> str:
+    return load().qkn_strerror(status).decode()
+
+
+def qkn_partial_sumsq(x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """Phase A: out[t] = sum_j x[t, j]^2 (fp32) for a bf16 [T, d_local] tensor."""
+    px, ldx, T, d = _rows(x, "x")
+    if out is None:
+        out = torch.empty(T, dtype=torch.float32, device=x.device)
+    po = _f32(out, "out", T)
+    _check(load().qkn_partial_sumsq(px, ldx, T, d, po, _stream(stream)), "qkn_partial_sumsq")
+    return out
+
+
+def qkn_apply(x: torch.Tensor, w: torch.Tensor, partials: torch.Tensor, d_full: int,
+              eps: float, y: Optional[torch.Tensor] = None,
+              inv_rms: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Phases B+C from all ranks' statistics: partials is fp32 [tp, T] (rank-major)."""
+    px, ldx, T, d = _rows(x, "x")
+    if partials.dim() != 2 or partials.shape[1] != T:
+        raise ValueError(f"partials: expected [tp, {T}], got {tuple(partials.shape)}")
+    tp = partials.shape[0]
+    if y is None:
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=x.device)
+    py, ldy, Ty, dy = _rows(y, "y")
+    if (Ty, dy) != (T, d):
+        raise ValueError("y: shape must match x")
+    _check(load().qkn_apply(px, ldx, _f32(w, "w", d), _f32(partials, "partials"), tp, T, d,
+                            d_full, eps, py, ldy, _f32(inv_rms, "inv_rms", T),
+                            _stream(stream)), "qkn_apply")
+    return y
+
+
+@dataclass
+class Seg:
+    """One tensor (Q or K) of one rank for qkn_fused_shard / qkn_full."""
+
+    x: torch.Tensor                  # bf16 [T, d_local] (row stride free)
+    w: torch.Tensor                  # fp32 [d_local]
+    d_full: int
+    y: Optional[torch.Tensor] = None  # bf16 [T, d_local]; allocated if None
+    partials: Optional[torch.Tensor] = None  # fp32 [tp, T]
+    inv_rms: Optional[torch.Tensor] = None   # fp32 [T]
+
+
+def _segs(segs: Sequence[Seg], tp: int):
+    arr = (QknSeg * len(segs))()
+    T = None
+    for i, s in enumerate(segs):
+        px, ldx, Ts, d = _rows(s.x, f"seg{i}.x")
+        if T is None:
+            T = Ts
+        elif Ts != T:
+            raise ValueError("all segments must have the same number of tokens")
+        if s.y is None:
+            s.y = torch.empty((Ts, d), dtype=torch.bfloat16, device=s.x.device)
+        py, ldy, Ty, dy = _rows(s.y, f"seg{i}.y")
+        if (Ty, dy) != (Ts, d):
+            raise ValueError(f"seg{i}.y: shape must match x")
+        pp = None
+        if s.partials is not None:
+            if s.partials.dim() != 2 or tuple(s.partials.shape) != (tp, Ts):
+                raise ValueError(f"seg{i}.partials: expected [{tp}, {Ts}]")
+            pp = _f32(s.partials, f"seg{i}.partials")
+        arr[i] = QknSeg(px, ldx, _f32(s.w, f"seg{i}.w", d), pp, py, ldy,
+                        _f32(s.inv_rms, f"seg{i}.inv_rms", Ts), d, s.d_full)
+    return arr, T
+
+
+def qkn_fused_shard(segs: Sequence[Seg], tp: int, rank: int, eps: float, stream=None):
+    """Fused Phases A+B+C for rank `rank` of `tp`, one launch for all segments."""
+    arr, T = _segs(segs, tp)
+    _check(load().qkn_fused_shard(arr, len(segs), tp, rank, T, eps, _stream(stream)),
+           "qkn_fused_shard")
+    return [s.y for s in segs]
+
+
+def qkn_full(segs: Sequence[Seg], eps: float, stream=None):
+    """TP = 1 full-vector QK-Norm (d_full == d_local for every segment)."""
+    arr, T = _segs(segs, 1)
+    _check(load().qkn_full(arr, len(segs), T, eps, _stream(stream)), "qkn_full")
+    return [s.y for s in segs]
+
+
+def qkn_last_launch() -> dict:
+    info = QknLaunchInfo()
+    _check(load().qkn_last_launch(ctypes.byref(info)), "qkn_last_launch")
+    return {"kernel": info.kernel.decode() if info.kernel else None, "grid": info.grid,
+            "block": info.block, "waves": info.waves, "lds_bytes": info.lds_bytes}
+
+
+def qkn_set_option(key: str, value: int) -> None:
+    _check(load().qkn_set_option(key.encode(), int(value)), f"qkn_set_option({key})")

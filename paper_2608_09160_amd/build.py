@@ -1,0 +1,56 @@
+"""Build libqkn.so (the HIP kernels and their C ABI) for gfx950, in-tree.
+
+    python -m paper_2608_09160_amd.build [--asm]
+
+The library is written to this package's directory so that it travels with
+the source tree. `--asm` also writes the gfx950 assembly next to it
+(libqkn-gfx950.s) for inspection of register use and instruction selection.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG_DIR)
+SRC = os.path.join(PKG_DIR, "csrc", "qkn.hip")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG_DIR, "libqkn.so")
+ARCH = "gfx950"
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+# Packed fp32 instructions are disabled for all device code: some of their forms
+# have produced wrong results on this hardware; plain fp32 code is unaffected.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+COMMON = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-I", INCLUDE, "-Wall",
+          "-Wno-unused-variable"] + DEVICE_FLAGS
+
+
+def _run(cmd):
+    proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    # the host pass does not know the device-only target feature; that warning is harmless
+    out = "\n".join(l for l in proc.stdout.splitlines()
+                    if "packed-fp32-ops" not in l and "not a recognized feature" not in l)
+    if proc.returncode != 0:
+        raise RuntimeError(f"build failed ({proc.returncode}): {' '.join(cmd)}\n{out}")
+    return out
+
+
+def build(asm: bool = False, verbose: bool = False) -> str:
+    """Compile libqkn.so (always recompiles). Returns the library path."""
+    tmp = LIB + ".tmp"
+    out = _run([HIPCC, *COMMON, "-shared", "-fPIC", "-o", tmp, SRC])
+    os.replace(tmp, LIB)
+    if verbose and out.strip():
+        print(out)
+    if asm:
+        _run([HIPCC, *COMMON, "--cuda-device-only", "-S", "-o",
+              os.path.join(PKG_DIR, f"libqkn-{ARCH}.s"), SRC])
+    return LIB
+
+
+if __name__ == "__main__":
+    path = build(asm="--asm" in sys.argv, verbose=True)
+    print(path)

@@ -1,0 +1,849 @@
+// libqkn: sharded layerwise QK-Norm for AMD MI355X (gfx950, CDNA4, wave64).
+//
+// What is computed (SwiftQK, arXiv 2608.09160): RMSNorm of Eq. 1 (Sec. II-A)
+// applied to each token's full projected Q and, separately, K vector, when the
+// hidden dimension is split over tensor-parallel ranks (Sec. II-B). One rank's
+// share follows the three phases of Sec. III / Alg. 1:
+//   Phase A  partial sum of squares of the rank's slice, fp32;
+//   Phase B  ascending-rank sum of all ranks' partials and the factor
+//            1/sqrt(S/H_total + eps); independently of it, x * gamma;
+//   Phase C  the scaled slice, rounded once to bf16 and written.
+//
+// Design for gfx950 (the paper's warp/block layout is prior art, not reused):
+//   * One wavefront owns one token at a time: its Q row and K row are spread
+//     over the 64 lanes in 16-byte chunks (8 bf16), chunk c on lane c % 64, so
+//     the row reduction needs no LDS and no barrier: four DPP row steps and
+//     four readlanes.
+//   * The rows stay in registers between Phase A and Phase C (one HBM read of
+//     x, one write of y); gamma is loaded into registers once per wavefront and
+//     reused for every token of the persistent loop.
+//   * The other ranks' statistics are fetched by lanes 0..tp-1 together with
+//     the row, so their latency overlaps Phase A and the x * gamma products.
+//   * The grid is persistent: at most (resident waves per CU) x (CU count)
+//     wavefronts, each striding over tokens (Sec. III-D bounds the grid the
+//     same way, there for deadlock safety across GPUs).
+//   * x and y are streamed with non-temporal 128-bit accesses.
+//   * A general kernel covers any width, stride and alignment with the same
+//     summation tree (so the same bits), staging the row in LDS.
+//
+// Summation tree of a row (fixed, depends only on d_local): lane l
+// accumulates, with fused multiply-adds in ascending column order, the
+// elements of chunks l, l+64, l+128, ...; the 16 lanes of each DPP row are then
+// combined by symmetric butterflies (every lane of a row ends with the same
+// bits) and the four row sums r0..r3 are added as (r0 + r1) + (r2 + r3).
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdio.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "qkn.h"
+
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr int kChunk = 8;           // bf16 elements per 128-bit access
+constexpr int kMaxRegChunks = 8;    // chunks per lane held in registers (d_local <= 4096)
+constexpr int kMaxFastTp = kWave;   // one statistic slot per lane
+constexpr int kMaxStageBytes = 64 * 1024;
+
+enum Mode { kFused = 0, kApply = 1, kPartial = 2 };
+
+struct DevSeg {
+  const uint16_t* x;
+  const float* w;
+  float* partials;  // [tp * T], rank-major
+  uint16_t* y;
+  float* inv_rms;   // optional [T]
+  int64_t ldx;
+  int64_t ldy;
+  int32_t d;        // d_local
+  int32_t nchunks;  // ceil(d_local / 8)
+  float d_full;     // divisor of the mean (H_total)
+  int32_t vec;      // 128-bit accesses allowed
+};
+
+struct KParams {
+  DevSeg seg[2];
+  int64_t T;
+  int32_t nseg;
+  int32_t tp;
+  int32_t rank;
+  float eps;
+};
+
+// ------------------------------------------------------------------ device helpers
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __builtin_bit_cast(float, u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __builtin_bit_cast(float, u & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
+}
+
+// Two fp32 values -> two bf16 (round to nearest even; v_cvt_pk_bf16_f32), low half first.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  return static_cast<uint16_t>(pack_bf16x2(f, 0.0f) & 0xffffu);
+}
+
+// Phase A on one 8-element chunk, ascending column order.
+__device__ __forceinline__ float chunk_sumsq(u32x4 v, float acc) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float a = bf16_lo(v[e]);
+    const float b = bf16_hi(v[e]);
+    acc = __builtin_fmaf(a, a, acc);
+    acc = __builtin_fmaf(b, b, acc);
+  }
+  return acc;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float read_lane(float v, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+
+// Sum over the 64 lanes; every lane must be active. Returns a wave-uniform value.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = v + dpp_move<0xB1>(v);   // quad_perm [1,0,3,2]: lane pairs
+  v = v + dpp_move<0x4E>(v);   // quad_perm [2,3,0,1]: quads
+  v = v + dpp_move<0x141>(v);  // row_half_mirror: 8 lanes
+  v = v + dpp_move<0x140>(v);  // row_mirror: 16 lanes
+  const float r0 = read_lane(v, 0), r1 = read_lane(v, 16);
+  const float r2 = read_lane(v, 32), r3 = read_lane(v, 48);
+  return (r0 + r1) + (r2 + r3);
+}
+
+// Lanes 0..tp-1 fetch rank k's slot of token t; the slot `skip` (the rank's
+// own, computed in this kernel) is not read.
+__device__ __forceinline__ float load_slots(const float* partials, int64_t T, int64_t t,
+                                            int lane, int tp, int skip) {
+  float v = 0.0f;
+  if (lane < tp && lane != skip) v = partials[static_cast<int64_t>(lane) * T + t];
+  return v;
+}
+
+// Phase B reduction: S = P_0 + P_1 + ... + P_{tp-1}, left to right in fp32,
+// with P_own taken from the register `own` (own < 0: every slot from memory).
+__device__ __forceinline__ float combine_slots(float slots, float own, int tp, int own_rank) {
+  float S = (own_rank == 0) ? own : read_lane(slots, 0);
+  for (int k = 1; k < tp; ++k) {
+    const float pk = (k == own_rank) ? own : read_lane(slots, k);
+    S = S + pk;
+  }
+  return S;
+}
+
+// tp > 64: slot k lives on lane k % 64 of batch k / 64; batches are fetched in turn.
+__device__ __forceinline__ float combine_slots_any(const float* partials, int64_t T, int64_t t,
+                                                   int lane, int tp, float own, int own_rank) {
+  float S = 0.0f;
+  for (int k0 = 0; k0 < tp; k0 += kWave) {
+    const int n = (tp - k0 < kWave) ? tp - k0 : kWave;
+    const int skip = (own_rank >= k0 && own_rank < k0 + n) ? own_rank - k0 : -1;
+    float v = 0.0f;
+    if (lane < n && lane != skip) v = partials[static_cast<int64_t>(k0 + lane) * T + t];
+    for (int i = 0; i < n; ++i) {
+      const float pk = (i == skip) ? own : read_lane(v, i);
+      S = (k0 == 0 && i == 0) ? pk : S + pk;
+    }
+  }
+  return S;
+}
+
+__device__ __forceinline__ float rms_inverse(float S, float d_full, float eps) {
+  return 1.0f / sqrtf(S / d_full + eps);
+}
+
+__device__ __forceinline__ int64_t wave_index() {
+  const int w = static_cast<int>(blockIdx.x) * static_cast<int>(blockDim.x / kWave) +
+                static_cast<int>(threadIdx.x / kWave);
+  return __builtin_amdgcn_readfirstlane(w);
+}
+
+// ------------------------------------------------------------------ register path
+
+template <int N>
+__device__ __forceinline__ void load_gamma(const DevSeg& s, int lane, f32x4 (&g)[N][2]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int c = i * kWave + lane;
+    if (c < s.nchunks) {
+      const f32x4* src = reinterpret_cast<const f32x4*>(s.w) + 2 * c;
+      g[i][0] = src[0];
+      g[i][1] = src[1];
+    } else {
+      g[i][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+      g[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void load_row(const DevSeg& s, int64_t t, int lane, u32x4 (&x)[N]) {
+  const u32x4* row = reinterpret_cast<const u32x4*>(s.x + t * s.ldx);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int c = i * kWave + lane;
+    x[i] = (c < s.nchunks) ? __builtin_nontemporal_load(row + c) : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int N>
+__device__ __forceinline__ float row_lane_sumsq(const u32x4 (&x)[N]) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < N; ++i) acc = chunk_sumsq(x[i], acc);
+  return acc;
+}
+
+// Phase B compute path: z = x * gamma, elementwise in fp32.
+template <int N>
+__device__ __forceinline__ void times_gamma(const u32x4 (&x)[N], const f32x4 (&g)[N][2],
+                                            float (&z)[N][8]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const f32x4& gg = g[i][e >> 1];
+      z[i][2 * e] = bf16_lo(x[i][e]) * gg[(2 * e) & 3];
+      z[i][2 * e + 1] = bf16_hi(x[i][e]) * gg[(2 * e + 1) & 3];
+    }
+  }
+}
+
+// Phase C: y = bf16(z * inv), non-temporal 128-bit stores.
+template <int N>
+__device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t t, int lane,
+                                             const float (&z)[N][8], float inv) {
+  u32x4* row = reinterpret_cast<u32x4*>(s.y + t * s.ldy);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int c = i * kWave + lane;
+    if (c < s.nchunks) {
+      u32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(z[i][2 * e] * inv, z[i][2 * e + 1] * inv);
+      __builtin_nontemporal_store(o, row + c);
+    }
+  }
+}
+
+template <int N0, int N1, int MODE>
+__global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
+  constexpr int M1 = N1 > 0 ? N1 : 1;
+  const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (blockDim.x / kWave);
+  const DevSeg& s0 = p.seg[0];
+  const DevSeg& s1 = p.seg[1];
+  const int own_rank = (MODE == kFused) ? p.rank : -1;
+
+  f32x4 g0[N0][2];
+  f32x4 g1[M1][2];
+  if constexpr (MODE != kPartial) {
+    load_gamma<N0>(s0, lane, g0);
+    if constexpr (N1 > 0) load_gamma<N1>(s1, lane, g1);
+  }
+
+  for (int64_t t = wave_index(); t < p.T; t += nwaves) {
+    u32x4 x0[N0];
+    u32x4 x1[M1];
+    load_row<N0>(s0, t, lane, x0);
+    if constexpr (N1 > 0) load_row<N1>(s1, t, lane, x1);
+
+    float slots0 = 0.0f, slots1 = 0.0f;
+    if constexpr (MODE != kPartial) {
+      if (p.tp > 1 || MODE == kApply) {
+        slots0 = load_slots(s0.partials, p.T, t, lane, p.tp, own_rank);
+        if constexpr (N1 > 0) slots1 = load_slots(s1.partials, p.T, t, lane, p.tp, own_rank);
+      }
+    }
+
+    // Phase A: per-lane partial sums (not needed when every slot is given).
+    float a0 = 0.0f, a1 = 0.0f;
+    if constexpr (MODE != kApply) {
+      a0 = row_lane_sumsq<N0>(x0);
+      if constexpr (N1 > 0) a1 = row_lane_sumsq<N1>(x1);
+    }
+
+    if constexpr (MODE == kPartial) {
+      const float own0 = wave_sum(a0);
+      if (lane == 0) s0.partials[t] = own0;
+    } else {
+      // Phase B, compute path: independent of the statistic.
+      float z0[N0][8];
+      float z1[M1][8];
+      times_gamma<N0>(x0, g0, z0);
+      if constexpr (N1 > 0) times_gamma<N1>(x1, g1, z1);
+
+      // Phase B, reduction path.
+      float own0 = 0.0f, own1 = 0.0f;
+      if constexpr (MODE == kFused) {
+        own0 = wave_sum(a0);
+        if constexpr (N1 > 0) own1 = wave_sum(a1);
+      }
+      const float S0 = combine_slots(slots0, own0, p.tp, own_rank);
+      const float inv0 = rms_inverse(S0, s0.d_full, p.eps);
+      float inv1 = 0.0f;
+      if constexpr (N1 > 0) {
+        const float S1 = combine_slots(slots1, own1, p.tp, own_rank);
+        inv1 = rms_inverse(S1, s1.d_full, p.eps);
+      }
+
+      // Phase C.
+      store_scaled<N0>(s0, t, lane, z0, inv0);
+      if constexpr (N1 > 0) store_scaled<N1>(s1, t, lane, z1, inv1);
+      if (lane == 0) {
+        if constexpr (MODE == kFused) {
+          if (s0.partials) s0.partials[static_cast<int64_t>(p.rank) * p.T + t] = own0;
+          if constexpr (N1 > 0) {
+            if (s1.partials) s1.partials[static_cast<int64_t>(p.rank) * p.T + t] = own1;
+          }
+        }
+        if (s0.inv_rms) s0.inv_rms[t] = inv0;
+        if constexpr (N1 > 0) {
+          if (s1.inv_rms) s1.inv_rms[t] = inv1;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ general path
+//
+// Any width, stride or alignment. One wavefront per token; each segment in turn.
+// Lane l handles chunks l, l+64, ... exactly as above (same tree, same bits).
+// The row is staged in LDS between Phase A and Phase C when it fits; each lane
+// reads back only the chunks it wrote, so no barrier is needed.
+
+template <int MODE>
+__global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage_elems) {
+  extern __shared__ __align__(16) uint16_t stage[];
+  const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
+  const int64_t nwaves = gridDim.x;
+  const int own_rank = (MODE == kFused) ? p.rank : -1;
+
+  for (int64_t t = wave_index(); t < p.T; t += nwaves) {
+    for (int si = 0; si < p.nseg; ++si) {
+      const DevSeg& s = p.seg[si];
+      const uint16_t* xrow = s.x + t * s.ldx;
+      const bool staged = (MODE == kFused) && (s.nchunks * kChunk <= stage_elems);
+
+      float own = 0.0f;
+      if constexpr (MODE != kApply) {
+        float a = 0.0f;
+        for (int c = lane; c < s.nchunks; c += kWave) {
+          if (s.vec) {
+            const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(xrow) + c);
+            a = chunk_sumsq(v, a);
+            if (staged) *reinterpret_cast<u32x4*>(stage + c * kChunk) = v;
+          } else {
+            for (int e = 0; e < kChunk; ++e) {
+              const int j = c * kChunk + e;
+              if (j < s.d) {
+                const uint16_t b = xrow[j];
+                const float f = bf16_to_f32(b);
+                a = __builtin_fmaf(f, f, a);
+                if (staged) stage[j] = b;
+              }
+            }
+          }
+        }
+        own = wave_sum(a);
+      }
+
+      if constexpr (MODE == kPartial) {
+        if (lane == 0) s.partials[t] = own;
+        continue;
+      } else {
+        float S;
+        if (p.tp <= kMaxFastTp) {
+          const float slots = (p.tp > 1 || MODE == kApply)
+                                  ? load_slots(s.partials, p.T, t, lane, p.tp, own_rank)
+                                  : 0.0f;
+          S = combine_slots(slots, own, p.tp, own_rank);
+        } else {
+          S = combine_slots_any(s.partials, p.T, t, lane, p.tp, own, own_rank);
+        }
+        const float inv = rms_inverse(S, s.d_full, p.eps);
+
+        uint16_t* yrow = s.y + t * s.ldy;
+        for (int c = lane; c < s.nchunks; c += kWave) {
+          if (s.vec) {
+            const u32x4 v = staged ? *reinterpret_cast<const u32x4*>(stage + c * kChunk)
+                                   : __builtin_nontemporal_load(
+                                         reinterpret_cast<const u32x4*>(xrow) + c);
+            const f32x4* gp = reinterpret_cast<const f32x4*>(s.w) + 2 * c;
+            const f32x4 ga = gp[0], gb = gp[1];
+            u32x4 o;
+            o[0] = pack_bf16x2((bf16_lo(v[0]) * ga[0]) * inv, (bf16_hi(v[0]) * ga[1]) * inv);
+            o[1] = pack_bf16x2((bf16_lo(v[1]) * ga[2]) * inv, (bf16_hi(v[1]) * ga[3]) * inv);
+            o[2] = pack_bf16x2((bf16_lo(v[2]) * gb[0]) * inv, (bf16_hi(v[2]) * gb[1]) * inv);
+            o[3] = pack_bf16x2((bf16_lo(v[3]) * gb[2]) * inv, (bf16_hi(v[3]) * gb[3]) * inv);
+            __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(yrow) + c);
+          } else {
+            for (int e = 0; e < kChunk; ++e) {
+              const int j = c * kChunk + e;
+              if (j < s.d) {
+                const uint16_t b = staged ? stage[j] : xrow[j];
+                const float z = bf16_to_f32(b) * s.w[j];
+                yrow[j] = f32_to_bf16(z * inv);
+              }
+            }
+          }
+        }
+        if (lane == 0) {
+          if constexpr (MODE == kFused) {
+            if (s.partials) s.partials[static_cast<int64_t>(p.rank) * p.T + t] = own;
+          }
+          if (s.inv_rms) s.inv_rms[t] = inv;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ host side
+
+typedef void (*RowsFn)(KParams);
+typedef void (*GenericFn)(KParams, int32_t);
+
+// Chunks per lane are rounded up to 1, 2, 4 or 8; unused chunks are masked.
+constexpr int kNIdx[9] = {-1, 0, 1, 2, 2, 3, 3, 3, 3};  // chunks/lane -> table index
+constexpr int kNVal[4] = {1, 2, 4, 8};
+
+#define QKN_ROW_SET(M, A)                                                              \
+  {qkn_rows<A, 0, M>, qkn_rows<A, 1, M>, qkn_rows<A, 2, M>, qkn_rows<A, 4, M>,         \
+   qkn_rows<A, 8, M>}
+
+// [N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
+const RowsFn kFusedTable[4][5] = {QKN_ROW_SET(kFused, 1), QKN_ROW_SET(kFused, 2),
+                                  QKN_ROW_SET(kFused, 4), QKN_ROW_SET(kFused, 8)};
+const RowsFn kApplyTable[4] = {qkn_rows<1, 0, kApply>, qkn_rows<2, 0, kApply>,
+                               qkn_rows<4, 0, kApply>, qkn_rows<8, 0, kApply>};
+const RowsFn kPartialTable[4] = {qkn_rows<1, 0, kPartial>, qkn_rows<2, 0, kPartial>,
+                                 qkn_rows<4, 0, kPartial>, qkn_rows<8, 0, kPartial>};
+const GenericFn kGenericTable[3] = {qkn_generic<kFused>, qkn_generic<kApply>,
+                                    qkn_generic<kPartial>};
+
+const char* const kModeName[3] = {"fused", "apply", "partial"};
+
+// Static names "rows<N0,N1>/mode" for the launch description.
+const char* rows_name(int mode, int i0, int i1) {
+  static char names[3][4][5][32];
+  static std::once_flag once;
+  std::call_once(once, [] {
+    for (int m = 0; m < 3; ++m)
+      for (int a = 0; a < 4; ++a)
+        for (int b = 0; b < 5; ++b)
+          snprintf(names[m][a][b], sizeof(names[m][a][b]), "rows<%d,%d>/%s", kNVal[a],
+                   b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
+  });
+  return names[mode][i0][i1];
+}
+const char* const kGenericName[3] = {"generic/fused", "generic/apply", "generic/partial"};
+
+// Options.
+int64_t g_opt_waves_per_cu = 0;
+int64_t g_opt_waves_per_block = 0;
+int64_t g_opt_force_generic = 0;
+int64_t g_opt_validate_only = 0;
+
+thread_local qkn_launch_info t_last = {nullptr, 0, 0, 0, 0};
+
+// Per-device CU count and per-kernel occupancy, filled on first use.
+constexpr int kMaxDevices = 64;
+struct OccEntry {
+  const void* fn;
+  int block;
+  int lds;
+  int blocks_per_cu;
+};
+struct DeviceCache {
+  int cu_count = 0;
+  OccEntry occ[256];
+  int nocc = 0;
+};
+std::mutex g_mu;
+DeviceCache g_dev[kMaxDevices];
+
+int query_device(int* dev, int* cu_count) {
+  if (hipGetDevice(dev) != hipSuccess || *dev < 0 || *dev >= kMaxDevices) return QKN_EHIP;
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceCache& dc = g_dev[*dev];
+  if (dc.cu_count == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, *dev) != hipSuccess ||
+        n <= 0)
+      return QKN_EHIP;
+    dc.cu_count = n;
+  }
+  *cu_count = dc.cu_count;
+  return QKN_OK;
+}
+
+int blocks_per_cu(int dev, const void* fn, int block, int lds, int* out) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceCache& dc = g_dev[dev];
+  for (int i = 0; i < dc.nocc; ++i) {
+    if (dc.occ[i].fn == fn && dc.occ[i].block == block && dc.occ[i].lds == lds) {
+      *out = dc.occ[i].blocks_per_cu;
+      return QKN_OK;
+    }
+  }
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds) != hipSuccess || n <= 0)
+    return QKN_EHIP;
+  if (dc.nocc < 256) dc.occ[dc.nocc++] = OccEntry{fn, block, lds, n};
+  *out = n;
+  return QKN_OK;
+}
+
+// ---------------------------------------------------------------- validation
+
+bool bad_eps(float eps) { return !(eps >= 0.0f) || !isfinite(eps); }
+
+// A strided byte region: `rows` rows of `width` elements every `ld` elements.
+struct Span {
+  uintptr_t base;
+  int64_t rows, ld, width, esz;
+};
+
+int64_t floor_div(int64_t a, int64_t b) {  // b > 0
+  int64_t q = a / b;
+  if ((a % b != 0) && ((a < 0) != (b < 0))) --q;
+  return q;
+}
+
+bool spans_overlap(const Span& a, const Span& b) {
+  if (a.rows <= 0 || b.rows <= 0 || a.width <= 0 || b.width <= 0) return false;
+  const __int128 a_lo = a.base, b_lo = b.base;
+  const __int128 a_hi = a_lo + ((__int128)(a.rows - 1) * a.ld + a.width) * a.esz;
+  const __int128 b_hi = b_lo + ((__int128)(b.rows - 1) * b.ld + b.width) * b.esz;
+  if (a_hi <= b_lo || b_hi <= a_lo) return false;  // disjoint extents
+  // Same element size and stride: exact test on element offsets.
+  if (a.esz == b.esz && a.ld == b.ld && a.ld > 0) {
+    const __int128 off_bytes = b_lo - a_lo;
+    if (off_bytes % a.esz == 0) {
+      const int64_t o = static_cast<int64_t>(off_bytes / a.esz);
+      const int64_t ld = a.ld;
+      // rows r of a and s of b overlap iff o - wa < (r - s) * ld < o + wb
+      const int64_t dmin = -(b.rows - 1), dmax = a.rows - 1;
+      int64_t d = floor_div(o - a.width, ld) + 1;
+      if (d < dmin) d = dmin;
+      return d <= dmax && (__int128)d * ld < (__int128)o + b.width;
+    }
+  }
+  return true;  // conservative
+}
+
+Span bf16_span(const void* p, int64_t rows, int64_t ld, int64_t width) {
+  return Span{reinterpret_cast<uintptr_t>(p), rows, ld, width, 2};
+}
+Span f32_span(const void* p, int64_t n) {
+  return Span{reinterpret_cast<uintptr_t>(p), 1, n, n, 4};
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int64_t kMaxWidth = (int64_t{1} << 30);  // d_local and strides fit in int32 chunk math
+
+struct Planned {
+  KParams kp;
+  int mode;
+};
+
+int check_seg_shape(const qkn_seg& s, int mode) {
+  if (!s.x) return QKN_EINVAL;
+  if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local) return QKN_EINVAL;
+  if (mode != kPartial) {
+    if (!s.w || !s.y) return QKN_EINVAL;
+    if (s.d_full < s.d_local || s.ldy < s.d_local) return QKN_EINVAL;
+  }
+  return QKN_OK;
+}
+
+// Overlap rules: outputs (y, own statistic slots, inv_rms) may not overlap any
+// input or another output, except y == x with equal strides (in place) and a
+// segment's own slots inside its own partials array.
+int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, int mode) {
+  struct Item {
+    Span s;
+    bool out;
+    int seg;
+    int kind;  // 0 x, 1 w, 2 partials (read), 3 y, 4 own slots, 5 inv
+  };
+  Item items[12];
+  int n = 0;
+  for (int i = 0; i < nseg; ++i) {
+    const qkn_seg& s = segs[i];
+    items[n++] = Item{bf16_span(s.x, T, s.ldx, s.d_local), false, i, 0};
+    if (mode == kPartial) {
+      items[n++] = Item{f32_span(s.partials, T), true, i, 4};
+      continue;
+    }
+    items[n++] = Item{f32_span(s.w, s.d_local), false, i, 1};
+    if (s.partials) {
+      if (mode == kApply || tp > 1) items[n++] = Item{f32_span(s.partials, tp * T), false, i, 2};
+      if (mode == kFused) items[n++] = Item{f32_span(s.partials + (int64_t)rank * T, T), true, i, 4};
+    }
+    items[n++] = Item{bf16_span(s.y, T, s.ldy, s.d_local), true, i, 3};
+    if (s.inv_rms) items[n++] = Item{f32_span(s.inv_rms, T), true, i, 5};
+  }
+  for (int a = 0; a < n; ++a) {
+    for (int b = a + 1; b < n; ++b) {
+      const Item& A = items[a];
+      const Item& B = items[b];
+      if (!A.out && !B.out) continue;
+      if (A.seg == B.seg) {
+        const int lo = A.kind < B.kind ? A.kind : B.kind;
+        const int hi = A.kind < B.kind ? B.kind : A.kind;
+        if (lo == 2 && hi == 4) continue;  // own slots live inside the partials array
+        if (lo == 0 && hi == 3 && A.s.base == B.s.base && A.s.ld == B.s.ld) continue;  // in place
+      }
+      if (spans_overlap(A.s, B.s)) return QKN_EOVERLAP;
+    }
+  }
+  return QKN_OK;
+}
+
+bool seg_vec_ok(const qkn_seg& s, int mode) {
+  if (!aligned16(s.x) || (s.ldx % kChunk) || (s.d_local % kChunk)) return false;
+  if (mode != kPartial) {
+    if (!aligned16(s.y) || !aligned16(s.w) || (s.ldy % kChunk)) return false;
+  }
+  return true;
+}
+
+DevSeg to_dev(const qkn_seg& s, int mode) {
+  DevSeg d;
+  d.x = s.x;
+  d.w = s.w;
+  d.partials = s.partials;
+  d.y = s.y;
+  d.inv_rms = s.inv_rms;
+  d.ldx = s.ldx;
+  d.ldy = (mode == kPartial) ? 0 : s.ldy;
+  d.d = static_cast<int32_t>(s.d_local);
+  d.nchunks = static_cast<int32_t>((s.d_local + kChunk - 1) / kChunk);
+  d.d_full = static_cast<float>(mode == kPartial ? s.d_local : s.d_full);
+  d.vec = seg_vec_ok(s, mode) ? 1 : 0;
+  return d;
+}
+
+int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps, int mode,
+           void* stream) {
+  KParams kp;
+  memset(&kp, 0, sizeof(kp));
+  kp.T = T;
+  kp.nseg = nseg;
+  kp.tp = tp;
+  kp.rank = rank;
+  kp.eps = eps;
+  bool fast = (g_opt_force_generic == 0) && tp <= kMaxFastTp;
+  int idx[2] = {0, 0};
+  int max_chunks = 0;
+  for (int i = 0; i < nseg; ++i) {
+    kp.seg[i] = to_dev(segs[i], mode);
+    const int per_lane = (kp.seg[i].nchunks + kWave - 1) / kWave;
+    if (!kp.seg[i].vec || per_lane > kMaxRegChunks) fast = false;
+    else idx[i] = kNIdx[per_lane];
+    if (kp.seg[i].nchunks > max_chunks) max_chunks = kp.seg[i].nchunks;
+  }
+
+  const void* fn;
+  const char* name;
+  int lds = 0;
+  int32_t stage_elems = 0;
+  if (fast) {
+    if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
+    else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[idx[0]]);
+    else fn = reinterpret_cast<const void*>(kPartialTable[idx[0]]);
+    name = rows_name(mode, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+  } else {
+    fn = reinterpret_cast<const void*>(kGenericTable[mode]);
+    name = kGenericName[mode];
+    if (mode == kFused && static_cast<int64_t>(max_chunks) * kChunk * 2 <= kMaxStageBytes) {
+      stage_elems = max_chunks * kChunk;
+      lds = stage_elems * 2;
+    }
+  }
+  if (g_opt_validate_only) {  // arguments accepted and a kernel chosen; no HIP call
+    t_last = qkn_launch_info{name, 0, 0, 0, lds};
+    return QKN_OK;
+  }
+
+  int dev = 0, cus = 0;
+  int rc = query_device(&dev, &cus);
+  if (rc != QKN_OK) return rc;
+  int wpb = 1;
+  if (fast) {
+    if (g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
+    else wpb = (T <= 4 * static_cast<int64_t>(cus)) ? 1 : 4;
+  }
+  const int block = wpb * kWave;
+  int bpc = 0;
+  rc = blocks_per_cu(dev, fn, block, lds, &bpc);
+  if (rc != QKN_OK) return rc;
+  int64_t waves_per_cu = static_cast<int64_t>(bpc) * wpb;
+  if (g_opt_waves_per_cu > 0 && g_opt_waves_per_cu < waves_per_cu) waves_per_cu = g_opt_waves_per_cu;
+  if (waves_per_cu < 1) waves_per_cu = 1;
+  int64_t waves = waves_per_cu * cus;
+  if (waves > T) waves = T;
+  int64_t grid = (waves + wpb - 1) / wpb;
+  if (grid > 0x7fffffff) grid = 0x7fffffff;
+
+  hipError_t err;
+  if (fast) {
+    void* args[] = {&kp};
+    err = hipLaunchKernel(fn, dim3(static_cast<unsigned>(grid)), dim3(block), args, 0,
+                          static_cast<hipStream_t>(stream));
+  } else {
+    void* args[] = {&kp, &stage_elems};
+    err = hipLaunchKernel(fn, dim3(static_cast<unsigned>(grid)), dim3(block), args, lds,
+                          static_cast<hipStream_t>(stream));
+  }
+  if (err != hipSuccess) return QKN_EHIP;
+  t_last = qkn_launch_info{name, grid, block, grid * wpb, lds};
+  return QKN_OK;
+}
+
+int validate_common(int64_t T, float eps, int tp, int rank) {
+  if (T < 0 || tp < 1 || rank < 0 || rank >= tp || bad_eps(eps)) return QKN_EINVAL;
+  if (T > 0 && static_cast<__int128>(T) * tp > INT64_MAX / 8) return QKN_EINVAL;
+  return QKN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qkn_partial_sumsq(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                      float* partial_out, void* stream) {
+  if (T < 0 || d_local < 1 || d_local > kMaxWidth || ldx < d_local) return QKN_EINVAL;
+  if (T == 0) return QKN_OK;
+  if (!x || !partial_out) return QKN_EINVAL;
+  qkn_seg s;
+  memset(&s, 0, sizeof(s));
+  s.x = x;
+  s.ldx = ldx;
+  s.partials = partial_out;
+  s.d_local = d_local;
+  s.d_full = d_local;
+  int rc = check_seg_shape(s, kPartial);
+  if (rc != QKN_OK) return rc;
+  rc = check_overlaps(&s, 1, 1, 0, T, kPartial);
+  if (rc != QKN_OK) return rc;
+  return launch(&s, 1, 1, 0, T, 0.0f, kPartial, stream);
+}
+
+int qkn_apply(const uint16_t* x, int64_t ldx, const float* w, const float* partials, int tp,
+              int64_t T, int64_t d_local, int64_t d_full, float eps, uint16_t* y, int64_t ldy,
+              float* inv_rms, void* stream) {
+  int rc = validate_common(T, eps, tp, 0);
+  if (rc != QKN_OK) return rc;
+  qkn_seg s;
+  s.x = x;
+  s.ldx = ldx;
+  s.w = w;
+  s.partials = const_cast<float*>(partials);
+  s.y = y;
+  s.ldy = ldy;
+  s.inv_rms = inv_rms;
+  s.d_local = d_local;
+  s.d_full = d_full;
+  if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
+      s.ldy < s.d_local)
+    return QKN_EINVAL;
+  if (T == 0) return QKN_OK;
+  rc = check_seg_shape(s, kApply);
+  if (rc != QKN_OK) return rc;
+  if (!partials) return QKN_EINVAL;
+  rc = check_overlaps(&s, 1, tp, 0, T, kApply);
+  if (rc != QKN_OK) return rc;
+  return launch(&s, 1, tp, 0, T, eps, kApply, stream);
+}
+
+int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
+                    void* stream) {
+  if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
+  int rc = validate_common(T, eps, tp, rank);
+  if (rc != QKN_OK) return rc;
+  for (int i = 0; i < nseg; ++i) {
+    const qkn_seg& s = segs[i];
+    if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
+        s.ldy < s.d_local)
+      return QKN_EINVAL;
+  }
+  if (T == 0) return QKN_OK;
+  for (int i = 0; i < nseg; ++i) {
+    rc = check_seg_shape(segs[i], kFused);
+    if (rc != QKN_OK) return rc;
+    if (tp > 1 && !segs[i].partials) return QKN_EINVAL;
+  }
+  rc = check_overlaps(segs, nseg, tp, rank, T, kFused);
+  if (rc != QKN_OK) return rc;
+  return launch(segs, nseg, tp, rank, T, eps, kFused, stream);
+}
+
+int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream) {
+  if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
+  for (int i = 0; i < nseg; ++i)
+    if (segs[i].d_full != segs[i].d_local) return QKN_EINVAL;
+  return qkn_fused_shard(segs, nseg, 1, 0, T, eps, stream);
+}
+
+const char* qkn_strerror(int status) {
+  switch (status) {
+    case QKN_OK: return "ok";
+    case QKN_EINVAL: return "invalid argument";
+    case QKN_EOVERLAP: return "output overlaps an input or another output";
+    case QKN_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int qkn_last_launch(qkn_launch_info* info) {
+  if (!info) return QKN_EINVAL;
+  *info = t_last;
+  return QKN_OK;
+}
+
+int qkn_set_option(const char* key, int64_t value) {
+  if (!key) return QKN_EINVAL;
+  if (strcmp(key, "waves_per_cu") == 0) {
+    if (value < 0 || value > 64) return QKN_EINVAL;
+    g_opt_waves_per_cu = value;
+  } else if (strcmp(key, "waves_per_block") == 0) {
+    if (value < 0 || value > 4) return QKN_EINVAL;
+    g_opt_waves_per_block = value;
+  } else if (strcmp(key, "force_generic") == 0) {
+    if (value != 0 && value != 1) return QKN_EINVAL;
+    g_opt_force_generic = value;
+  } else if (strcmp(key, "validate_only") == 0) {
+    if (value != 0 && value != 1) return QKN_EINVAL;
+    g_opt_validate_only = value;
+  } else {
+    return QKN_EINVAL;
+  }
+  return QKN_OK;
+}
+
+}  // extern "C"

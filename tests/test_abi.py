@@ -1,0 +1,231 @@
+"""The C ABI without a GPU: symbols, validation, overlap rules and path choice.
+
+Every call here either fails validation (which happens before any HIP call) or
+runs with the library's "validate_only" option set, which accepts the call and
+chooses a kernel without touching the GPU. The pointers are fake addresses that
+are never dereferenced, so these tests are safe on any machine.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_09160_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "qkn.h")
+
+BASE = 0x7f0000000000  # fake, 256-byte aligned device addresses
+MB = 1 << 20
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.load()
+
+
+@pytest.fixture
+def dry(lib):
+    assert lib.qkn_set_option(b"validate_only", 1) == 0
+    yield lib
+    assert lib.qkn_set_option(b"validate_only", 0) == 0
+    assert lib.qkn_set_option(b"force_generic", 0) == 0
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qkn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(lib):
+    names = _declared_functions()
+    assert set(names) >= {"qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
+                          "qkn_strerror", "qkn_last_launch", "qkn_set_option"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_strerror(lib):
+    for code in (0, -1, -2, -3, 17):
+        assert isinstance(lib.qkn_strerror(code), bytes)
+    assert lib.qkn_strerror(-2).startswith(b"output overlaps")
+
+
+def _seg(x, ldx, w, partials, y, ldy, d_local, d_full, inv=None):
+    return L.QknSeg(x, ldx, w, partials, y, ldy, inv, d_local, d_full)
+
+
+def _fused(lib, segs, tp, rank, T, eps=1e-6):
+    arr = (L.QknSeg * len(segs))(*segs)
+    return lib.qkn_fused_shard(arr, len(segs), tp, rank, T, ctypes.c_float(eps), None)
+
+
+def _q(T=64, d=1024, ld=None, rank_tp=4):
+    """A well-formed Q segment at distinct fake addresses."""
+    ld = ld or d
+    return _seg(BASE, ld, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, ld, d, d * rank_tp)
+
+
+def _k(T=64, d=256, rank_tp=4):
+    return _seg(BASE + 256 * MB, d, BASE + 300 * MB, BASE + 301 * MB, BASE + 400 * MB, d, d,
+                d * rank_tp)
+
+
+def test_valid_calls_pass_validation(dry):
+    assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
+    info = L.qkn_last_launch()
+    assert info["kernel"] == "rows<2,1>/fused" and info["grid"] == 0
+    assert dry.qkn_partial_sumsq(BASE, 1024, 64, 1024, BASE + 64 * MB, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/partial"
+    assert dry.qkn_apply(BASE, 1024, BASE + 64 * MB, BASE + 65 * MB, 4, 64, 1024, 4096,
+                         ctypes.c_float(1e-6), BASE + 128 * MB, 1024, None, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/apply"
+    full = [_seg(BASE, 4096, BASE + 64 * MB, 0, BASE + 128 * MB, 4096, 4096, 4096),
+            _seg(BASE + 256 * MB, 1024, BASE + 300 * MB, 0, BASE + 400 * MB, 1024, 1024, 1024)]
+    arr = (L.QknSeg * 2)(*full)
+    assert dry.qkn_full(arr, 2, 8192, ctypes.c_float(1e-6), None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<8,2>/fused"
+
+
+@pytest.mark.parametrize("d,expect", [(8, "rows<1,0>"), (512, "rows<1,0>"), (520, "rows<2,0>"),
+                                      (2048, "rows<4,0>"), (1536, "rows<4,0>"),
+                                      (4096, "rows<8,0>"), (4104, "generic"),
+                                      (100, "generic"), (1, "generic")])
+def test_path_choice_by_width(dry, d, expect):
+    seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
+    assert _fused(dry, [seg], 2, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"].startswith(expect)
+
+
+def test_path_choice_alignment_and_options(dry):
+    # misaligned x (one element off) or a stride that is not a multiple of 8
+    seg = _seg(BASE + 2, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 4096)
+    assert _fused(dry, [seg], 4, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    seg = _seg(BASE, 1028, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 4096)
+    assert _fused(dry, [seg], 4, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    seg = _seg(BASE, 1024, BASE + 64 * MB + 4, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 4096)
+    assert _fused(dry, [seg], 4, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    # tp beyond one slot per lane
+    assert _fused(dry, [_q(rank_tp=65)], 65, 64, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    # forced general path
+    assert dry.qkn_set_option(b"force_generic", 1) == 0
+    assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    assert L.qkn_last_launch()["lds_bytes"] == 1024 * 2
+
+
+def test_zero_tokens_is_a_noop(lib):
+    # T == 0 returns before any HIP call, even with NULL pointers
+    assert lib.qkn_partial_sumsq(None, 8, 0, 8, None, None) == 0
+    assert lib.qkn_apply(None, 8, None, None, 2, 0, 8, 16, ctypes.c_float(0.0),
+                         None, 8, None, None) == 0
+    seg = _seg(None, 8, None, None, None, 8, 8, 16)
+    assert _fused(lib, [seg], 2, 0, 0) == 0
+
+
+@pytest.mark.parametrize("case", [
+    "T<0", "tp<1", "rank>=tp", "rank<0", "eps<0", "eps=nan", "eps=inf", "nseg=0", "nseg=3",
+    "d_local<1", "ldx<d", "ldy<d", "d_full<d", "x=NULL", "w=NULL", "y=NULL", "partials=NULL",
+    "segs=NULL"])
+def test_invalid_arguments(lib, case):
+    q, k = _q(), _k()
+    tp, rank, T, eps, nseg = 4, 1, 64, 1e-6, 2
+    if case == "T<0": T = -1
+    elif case == "tp<1": tp = 0
+    elif case == "rank>=tp": rank = 4
+    elif case == "rank<0": rank = -1
+    elif case == "eps<0": eps = -1e-6
+    elif case == "eps=nan": eps = float("nan")
+    elif case == "eps=inf": eps = float("inf")
+    elif case == "nseg=0": nseg = 0
+    elif case == "nseg=3": nseg = 3
+    elif case == "d_local<1": q.d_local = 0
+    elif case == "ldx<d": q.ldx = 1000
+    elif case == "ldy<d": k.ldy = 255
+    elif case == "d_full<d": k.d_full = 255
+    elif case == "x=NULL": q.x = None
+    elif case == "w=NULL": k.w = None
+    elif case == "y=NULL": q.y = None
+    elif case == "partials=NULL": k.partials = None
+    arr = (L.QknSeg * 3)(q, k, k)
+    ptr = None if case == "segs=NULL" else arr
+    rc = lib.qkn_fused_shard(ptr, nseg, tp, rank, T, ctypes.c_float(eps), None)
+    assert rc == L.QKN_EINVAL
+
+
+def test_invalid_partial_and_apply(lib):
+    f = ctypes.c_float
+    assert lib.qkn_partial_sumsq(BASE, 8, 4, 0, BASE + MB, None) == L.QKN_EINVAL
+    assert lib.qkn_partial_sumsq(BASE, 8, 4, 16, BASE + MB, None) == L.QKN_EINVAL
+    assert lib.qkn_partial_sumsq(None, 8, 4, 8, BASE + MB, None) == L.QKN_EINVAL
+    assert lib.qkn_partial_sumsq(BASE, 8, 4, 8, None, None) == L.QKN_EINVAL
+    assert lib.qkn_partial_sumsq(BASE, 8, -1, 8, BASE + MB, None) == L.QKN_EINVAL
+    ok = dict(x=BASE, ldx=8, w=BASE + MB, p=BASE + 2 * MB, tp=2, T=4, d=8, dfull=16, eps=1e-6,
+              y=BASE + 3 * MB, ldy=8)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.qkn_apply(a["x"], a["ldx"], a["w"], a["p"], a["tp"], a["T"], a["d"],
+                             a["dfull"], f(a["eps"]), a["y"], a["ldy"], None, None)
+    for bad in (dict(p=None), dict(w=None), dict(y=None), dict(x=None), dict(tp=0),
+                dict(dfull=7), dict(ldy=7), dict(eps=-1.0), dict(T=-3)):
+        assert call(**bad) == L.QKN_EINVAL, bad
+    # full-vector call requires d_local == d_full
+    seg = _seg(BASE, 8, BASE + MB, None, BASE + 3 * MB, 8, 8, 16)
+    assert lib.qkn_full((L.QknSeg * 1)(seg), 1, 4, f(1e-6), None) == L.QKN_EINVAL
+
+
+def test_overlap_rules(dry):
+    T, d = 16, 1024
+    # y shifted by one element onto x: partial overlap
+    seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 2, d, d, 2 * d)
+    assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
+    # exactly in place: allowed
+    seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE, d, d, 2 * d)
+    assert _fused(dry, [seg], 2, 0, T) == 0
+    # in place but a different stride: rejected
+    seg = _seg(BASE, 2 * d, BASE + 64 * MB, BASE + 65 * MB, BASE, d, d, 2 * d)
+    assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
+    # Q and K as column slices of one packed buffer, written in place: disjoint columns
+    ld = 1024 + 256 + 256
+    q = _seg(BASE, ld, BASE + 64 * MB, BASE + 65 * MB, BASE, ld, 1024, 4096)
+    k = _seg(BASE + 2 * 1024, ld, BASE + 66 * MB, BASE + 67 * MB, BASE + 2 * 1024, ld, 256, 1024)
+    assert _fused(dry, [q, k], 4, 3, T) == 0
+    # K's output written over Q's input columns: rejected
+    k = _seg(BASE + 2 * 1024, ld, BASE + 66 * MB, BASE + 67 * MB, BASE + 2 * 512, ld, 256, 1024)
+    assert _fused(dry, [q, k], 4, 3, T) == L.QKN_EOVERLAP
+    # both segments sharing one partials array: their own slots collide
+    q = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
+    k = _seg(BASE + 256 * MB, 256, BASE + 300 * MB, BASE + 65 * MB, BASE + 400 * MB, 256, 256, 512)
+    assert _fused(dry, [q, k], 2, 0, T) == L.QKN_EOVERLAP
+    # ...but one array holding [2][tp][T] (disjoint per segment) is fine
+    k = _seg(BASE + 256 * MB, 256, BASE + 300 * MB, BASE + 65 * MB + 2 * T * 4, BASE + 400 * MB,
+             256, 256, 512)
+    assert _fused(dry, [q, k], 2, 0, T) == 0
+    # inv_rms over the partials array
+    q = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d,
+             inv=BASE + 65 * MB + 8)
+    assert _fused(dry, [q], 2, 0, T) == L.QKN_EOVERLAP
+    # partial_out over x
+    assert dry.qkn_partial_sumsq(BASE, d, T, d, BASE + 100, None) == L.QKN_EOVERLAP
+    # y rows interleaved with x rows (same stride, column-disjoint): allowed
+    seg = _seg(BASE, 2 * d, BASE + 64 * MB, BASE + 65 * MB, BASE + 2 * d, 2 * d, d, 2 * d)
+    assert _fused(dry, [seg], 2, 0, T) == 0
+    # ...shifted by one column: overlaps
+    seg = _seg(BASE, 2 * d, BASE + 64 * MB, BASE + 65 * MB, BASE + 2 * (d - 1), 2 * d, d, 2 * d)
+    assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
+
+
+def test_options(lib):
+    assert lib.qkn_set_option(b"waves_per_cu", 8) == 0
+    assert lib.qkn_set_option(b"waves_per_cu", 0) == 0
+    assert lib.qkn_set_option(b"waves_per_cu", -1) == L.QKN_EINVAL
+    assert lib.qkn_set_option(b"waves_per_block", 5) == L.QKN_EINVAL
+    assert lib.qkn_set_option(b"no_such_key", 1) == L.QKN_EINVAL
+    assert lib.qkn_set_option(None, 1) == L.QKN_EINVAL

@@ -16,6 +16,9 @@ Recipe (shared by every workload):
   * one ``numpy.random.Generator`` per stream, seeded with
     ``SeedSequence([seed, stream_id])``; stream ids: 0 = X_Q, 1 = X_K,
     2 = per-token scales, 3 = outlier channels, 4 = gamma_Q, 5 = gamma_K;
+    the activations X_Q and X_K are drawn in blocks of 1024 tokens, block b
+    from ``SeedSequence([seed, stream_id, b])``, so blocks can be drawn in
+    parallel and the bits do not depend on the number of threads;
   * activations are drawn in fp32, shaped by the workload's distribution,
     then rounded to bf16 with round-to-nearest-even; everyone consumes the
     same bf16 bits;
@@ -29,10 +32,14 @@ Recipe (shared by every workload):
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, replace
 from typing import Dict, Tuple
 
 import numpy as np
+
+BLOCK_TOKENS = 1024
 
 STREAM_XQ, STREAM_XK, STREAM_SCALE, STREAM_OUTLIER, STREAM_GQ, STREAM_GK = range(6)
 
@@ -104,23 +111,48 @@ def _rng(seed: int, stream: int) -> np.random.Generator:
     return np.random.default_rng(np.random.SeedSequence([seed, stream]))
 
 
+def _threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def _activations(wl: Workload, d_full: int, stream: int, scale_col: int) -> np.ndarray:
-    rng = _rng(wl.seed, stream)
+    """bf16 bits [T, d_full] of one tensor, drawn block by block."""
+    if wl.dist not in ("normal", "student_t", "normal_lognormal", "normal_outliers"):
+        raise ValueError(f"unknown distribution {wl.dist!r}")
     T = wl.T
-    if wl.dist == "student_t":
-        x = rng.standard_t(wl.df, size=(T, d_full)).astype(np.float32)
-    else:
-        x = rng.standard_normal(size=(T, d_full), dtype=np.float32)
+    scale = None
     if wl.dist == "normal_lognormal":
         # one scale per token per tensor; column 0 = Q, column 1 = K
         s = np.exp(_rng(wl.seed, STREAM_SCALE).normal(0.0, wl.sigma, size=(T, 2)))
-        x *= s[:, scale_col:scale_col + 1].astype(np.float32)
-    elif wl.dist == "normal_outliers":
-        idx = outlier_channels(wl)[scale_col]
-        x[:, idx] *= np.float32(50.0)
-    elif wl.dist not in ("normal", "student_t"):
-        raise ValueError(f"unknown distribution {wl.dist!r}")
-    return x
+        scale = s[:, scale_col:scale_col + 1].astype(np.float32)
+    idx = outlier_channels(wl)[scale_col] if wl.dist == "normal_outliers" else None
+    out = np.empty((T, d_full), dtype=np.uint16)
+
+    def block(b: int) -> None:
+        t0, t1 = b * BLOCK_TOKENS, min(T, (b + 1) * BLOCK_TOKENS)
+        rng = np.random.default_rng(np.random.SeedSequence([wl.seed, stream, b]))
+        if wl.dist == "student_t":
+            x = rng.standard_t(wl.df, size=(t1 - t0, d_full)).astype(np.float32)
+        else:
+            x = rng.standard_normal(size=(t1 - t0, d_full), dtype=np.float32)
+        if scale is not None:
+            x *= scale[t0:t1]
+        if idx is not None:
+            x[:, idx] *= np.float32(50.0)
+        out[t0:t1] = f32_to_bf16_bits(x)
+
+    nblocks = (T + BLOCK_TOKENS - 1) // BLOCK_TOKENS
+    if nblocks <= 1:
+        for b in range(nblocks):
+            block(b)
+    else:
+        with ThreadPoolExecutor(min(_threads(), nblocks)) as ex:
+            list(ex.map(block, range(nblocks)))
+    return out
 
 
 def outlier_channels(wl: Workload) -> Tuple[np.ndarray, np.ndarray]:
@@ -141,8 +173,8 @@ def generate(wl: Workload) -> Dict[str, np.ndarray]:
     Returns ``xq`` uint16 [T, q_full], ``xk`` uint16 [T, k_full] (bf16 bits),
     ``gq`` float32 [q_full], ``gk`` float32 [k_full].
     """
-    xq = f32_to_bf16_bits(_activations(wl, wl.q_full, STREAM_XQ, 0))
-    xk = f32_to_bf16_bits(_activations(wl, wl.k_full, STREAM_XK, 1))
+    xq = _activations(wl, wl.q_full, STREAM_XQ, 0)
+    xk = _activations(wl, wl.k_full, STREAM_XK, 1)
     gq = _rng(wl.seed, STREAM_GQ).uniform(0.5, 1.5, size=wl.q_full).astype(np.float32)
     gk = _rng(wl.seed, STREAM_GK).uniform(0.5, 1.5, size=wl.k_full).astype(np.float32)
     return {"xq": xq, "xk": xk, "gq": gq, "gk": gk}
