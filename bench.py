@@ -47,6 +47,11 @@ def parse():
     p.add_argument("--no-extras", action="store_true",
                    help="only the headline workload (for profiler runs)")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--summarize", metavar="DIR",
+                   help="print summaries of rocprofv3 CSV output in DIR and exit")
+    p.add_argument("--calibration-copy", action="store_true",
+                   help="also run a plain device copy of Q's input (known bytes) a few times, "
+                        "to scale profiler byte counters")
     return p.parse_args()
 
 
@@ -97,50 +102,180 @@ class Case:
                                   y=torch.empty_like(x),
                                   partials=(P.clone() if i else P) if P is not None else None))
             self.sets.append(segs)
+        full = tp == 1 and not partials
+        self.calls = [L.Prepared(segs, tp, rank, wl.eps, full=full) for segs in self.sets]
         torch.cuda.synchronize()
         self.footprint = self.nsets * set_bytes
         self.bytes = algorithmic_bytes(T, (wl.q_local, wl.k_local), tp, write_partials=P is not None)
 
-    def launch(self, i, fn="fused"):
-        segs = self.sets[i % self.nsets]
-        if fn == "fused":
-            self.L.qkn_fused_shard(segs, self.wl.tp, self.rank, self.wl.eps)
-        elif fn == "full":
-            self.L.qkn_full(segs, self.wl.eps)
-        elif fn == "two_step":
-            for s in segs:
-                self.L.qkn_partial_sumsq(s.x, out=s.partials[self.rank])
-                self.L.qkn_apply(s.x, s.w, s.partials, s.d_full, self.wl.eps, y=s.y)
-        else:
-            raise ValueError(fn)
+    def launch(self, i):
+        self.calls[i % self.nsets]()
+
+    def launch_two_step(self, i):
+        """Phase A, then Phases B+C, per tensor: the unfused scalar-statistic path."""
+        for s in self.sets[i % self.nsets]:
+            self.L.qkn_partial_sumsq(s.x, out=s.partials[self.rank])
+            self.L.qkn_apply(s.x, s.w, s.partials, s.d_full, self.wl.eps, y=s.y)
 
 
-def time_launches(torch, fn, steps, warmup, per_launch=True):
-    """Run `fn(i)` warmup + steps times on the current stream.
-
-    Returns (region_ms, per_launch_ms list): the whole timed region between
-    two events, and each launch's own duration between events recorded right
-    before and after it (on the same stream)."""
+def time_region(torch, fn, steps, warmup):
+    """Wall time (ms) of `steps` back-to-back calls between two events on the stream."""
     stream = torch.cuda.current_stream()
     for i in range(warmup):
         fn(i)
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)] if per_launch else []
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for i in range(steps):
-        if per_launch:
-            ev[i][0].record(stream)
         fn(warmup + i)
-        if per_launch:
-            ev[i][1].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
-    region = start.elapsed_time(end)
-    each = [a.elapsed_time(b) for a, b in ev]
-    return region, each
+    return start.elapsed_time(end)
+
+
+def time_each(torch, fn, steps, warmup):
+    """Per-call durations (ms) from events recorded right before and after each call."""
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        fn(i)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        fn(warmup + i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def time_launches(torch, fn, steps, warmup):
+    """(region ms, per-call ms list) -- per-call events inside one timed region."""
+    stream = torch.cuda.current_stream()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    start.record(stream)
+    for i in range(steps):
+        ev[i][0].record(stream)
+        fn(warmup + i)
+        ev[i][1].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end), [a.elapsed_time(b) for a, b in ev]
+
+
+def time_graph(torch, fn, per_graph, replays):
+    """Mean time (ms) per call when `per_graph` calls are replayed from one HIP graph."""
+    fn(0)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            for i in range(per_graph):
+                fn(i)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    stream = torch.cuda.current_stream()
+    start.record(stream)
+    for _ in range(replays):
+        g.replay()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / (per_graph * replays)
+
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_09160_amd", "csrc", "qkn.hip")
+
+
+def source_sha256() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def counters_path(kernel: str, workload: str) -> str:
+    tag = kernel.replace("<", "_").replace(">", "").replace(",", "_").replace("/", "_")
+    return os.path.join(ROOT, "profiles", f"counters_{tag}_{workload}.txt")
+
+
+def traffic_bytes(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    there is none or the kernel source changed since the counters were taken."""
+    path = counters_path(kernel, workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_sha256():
+        return None
+    try:
+        return int(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def summarize(outdir: str, workload: str) -> None:
+    """Write profile summaries from rocprofv3 CSV output in `outdir`:
+    trace/*_kernel_trace.csv (kernel trace of the default bench run) and
+    pmc_fetch/*_counter_collection.csv, pmc_write/*_counter_collection.csv
+    (FETCH_SIZE / WRITE_SIZE runs with --no-extras --calibration-copy)."""
+    import csv
+    import glob
+    import statistics
+    trace = glob.glob(os.path.join(outdir, "trace", "*_kernel_trace.csv"))[0]
+    rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
+    runs = []  # consecutive dispatches of one kernel and launch shape
+    for r in rows:
+        name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+        key = (name, int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
+        d = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        if runs and runs[-1][0] == key:
+            runs[-1][1].append(d)
+        else:
+            runs.append([key, [d]])
+    head = ["| kernel | grid (threads) | workgroup | dispatches | mean us | median us | min us | max us |",
+            "|---|---|---|---|---|---|---|---|"]
+
+    def row(name, g, w, ds):
+        sd = sorted(ds)
+        return (f"| {name} | {g} | {w} | {len(ds)} | {statistics.mean(ds) / 1e3:.3f} | "
+                f"{sd[len(sd) // 2] / 1e3:.3f} | {sd[0] / 1e3:.3f} | {sd[-1] / 1e3:.3f} |")
+    print("Runs of at least 5 consecutive dispatches of one kernel and shape, in order:\n")
+    print("\n".join(head + [row(*k, ds) for k, ds in runs if len(ds) >= 5]))
+    total = {}
+    for k, ds in runs:
+        total.setdefault(k, []).extend(ds)
+    print("\nAll dispatches per kernel and shape:\n")
+    print("\n".join(head + [row(*k, ds) for k, ds in sorted(total.items(), key=lambda kv: -sum(kv[1]))]))
+
+    def counter(sub):
+        f = glob.glob(os.path.join(outdir, sub, "*_counter_collection.csv"))[0]
+        by = {}
+        for r in csv.DictReader(open(f)):
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            by.setdefault(name, []).append(float(r["Counter_Value"]))
+        return by
+    fetch, write = counter("pmc_fetch"), counter("pmc_write")
+    # calibration: the largest plain device copy (Q's input, known bytes)
+    cal_f = max(fetch["__amd_rocclr_copyBuffer"])
+    cal_w = max(write["__amd_rocclr_copyBuffer"])
+    print(f"\ncalibration copy: FETCH_SIZE {cal_f:.1f} KiB, WRITE_SIZE {cal_w:.1f} KiB")
+    for name in fetch:
+        if not name.startswith("void qkn_rows"):
+            continue
+        print(f"{name}: FETCH_SIZE {statistics.mean(fetch[name]):.1f} KiB, "
+              f"WRITE_SIZE {statistics.mean(write[name]):.1f} KiB per dispatch")
 
 
 def cpu_baseline(wl, rank, data, seconds):
@@ -171,6 +306,9 @@ def cpu_baseline(wl, rank, data, seconds):
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args.summarize, args.workload)
+        return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU's share of the sharded QK-Norm; the peer ranks "
@@ -194,71 +332,76 @@ def main():
     case = Case(wl, args.rank, min_fp, torch, L, workloads, data=data)
     case.launch(0)
     info = L.qkn_last_launch()
-    region_ms, each = time_launches(torch, case.launch, args.steps, args.warmup)
+    # timed region: exactly `steps` launches, nothing else on the stream
+    torch.cuda.synchronize()
+    region_ms = time_region(torch, case.launch, args.steps, args.warmup)
+    torch.cuda.synchronize()
     ms_per_step = region_ms / args.steps
-    kernel_ms = float(np.mean(each))
     value = case.bytes / (ms_per_step * 1e-3) / 1e9
+    # average launch duration = timed region / launches (back-to-back on one
+    # stream, as the profiler's kernel trace sees them)
+    kernel_ms = ms_per_step
     achieved = case.bytes / (kernel_ms * 1e-3) / 1e9
-    print(f"[bench] fused: {ms_per_step * 1e3:.2f} us/step, kernel {kernel_ms * 1e3:.2f} us "
-          f"({achieved:.0f} GB/s)", file=sys.stderr, flush=True)
+    # for reference: events bracketing every launch (adds the events' own cost)
+    each = time_each(torch, case.launch, args.steps, args.warmup)
+    isolated_ms = float(np.mean(each))
+    print(f"[bench] fused: {ms_per_step * 1e3:.2f} us/step ({achieved:.0f} GB/s); "
+          f"isolated launch {isolated_ms * 1e3:.2f} us", file=sys.stderr, flush=True)
 
     extras = {}
+    if args.calibration_copy:
+        xq, yq = case.sets[0][0].x, case.sets[0][0].y
+        for _ in range(5):
+            yq.copy_(xq)
+        torch.cuda.synchronize()
+        extras["calibration_copy"] = {"read_bytes": xq.numel() * 2, "write_bytes": yq.numel() * 2,
+                                      "launches": 5}
     if not args.no_extras:
-        # plain copy of the same number of bytes (x -> y of both tensors)
-        src = [s.x for s in case.sets[0]]
-        dst = [torch.empty_like(x) for x in src]
-        copy_bytes = sum(2 * x.numel() * 2 for x in src)
+        # plain copy of the same bytes (x -> y of both tensors), torch's copy kernel
         csets = [([s.x for s in segs], [s.y for s in segs]) for segs in case.sets]
 
         def copy(i):
             xs, ys = csets[i % len(csets)]
             for a, b in zip(xs, ys):
                 b.copy_(a)
-        r, e = time_launches(torch, copy, args.steps, args.warmup)
-        extras["copy_same_bytes"] = {"bytes": copy_bytes, "kernel_us": round(np.mean(e) * 1e3 / 2, 3),
-                                     "gbs_per_step": round(copy_bytes / (r / args.steps * 1e-3) / 1e9, 1)}
-        del src, dst
+        r = time_region(torch, copy, args.steps, args.warmup)
+        copy_bytes = sum(2 * s.x.numel() * 2 for s in case.sets[0])
+        extras["copy_same_bytes"] = {"bytes": copy_bytes, "us_per_step": round(r / args.steps * 1e3, 3),
+                                     "gbs": round(copy_bytes / (r / args.steps * 1e-3) / 1e9, 1)}
         # two launches per tensor: Phase A, then Phases B+C (x read twice)
-        r, e = time_launches(torch, lambda i: case.launch(i, "two_step"), args.steps, args.warmup)
+        r = time_region(torch, case.launch_two_step, args.steps, args.warmup)
         two_bytes = case.bytes + sum(2 * s.x.numel() for s in case.sets[0])
         extras["two_step_same_workload"] = {"us_per_step": round(r / args.steps * 1e3, 3),
                                             "gbs": round(two_bytes / (r / args.steps * 1e-3) / 1e9, 1),
                                             "bytes": two_bytes}
         # full-vector (tp = 1) baseline on the same tokens
-        full_wl = wl.with_tp(1)
-        fcase = Case(full_wl, 0, min_fp, torch, L, workloads, data=data, partials=False)
-        r, e = time_launches(torch, lambda i: fcase.launch(i, "full"), args.steps, args.warmup)
-        fk = float(np.mean(e))
+        fcase = Case(wl.with_tp(1), 0, min_fp, torch, L, workloads, data=data, partials=False)
+        fk = time_region(torch, fcase.launch, args.steps, args.warmup) / args.steps
         extras["full_vector_tp1"] = {"kernel": L.qkn_last_launch()["kernel"], "bytes": fcase.bytes,
                                      "kernel_us": round(fk * 1e3, 3),
                                      "gbs": round(fcase.bytes / (fk * 1e-3) / 1e9, 1)}
         del fcase
-        # decode shapes: latency of one launch, warm (inputs just produced, cache
-        # resident) and cold (rotating sets)
+        # decode shapes: one launch replayed from a HIP graph (inputs cache-warm,
+        # as right after the projection that produced them)
         lat = {}
         for name in ("decode_T64_q4096_k1024_tp4", "decode_T256_q5120_k1024_tp8",
                      "tiny_full_T16_q512_k128_tp1"):
             dwl = workloads.WORKLOADS[name]
             dcase = Case(dwl, 0, 0, torch, L, workloads, partials=dwl.tp > 1)
-            fn = (lambda i, c=dcase: c.launch(i, "full")) if dwl.tp == 1 else dcase.launch
-            r, e = time_launches(torch, lambda i, f=fn: f(0), 2000, 100)
-            lat[name] = {"us_median": round(float(np.median(e)) * 1e3, 3),
-                         "us_p10": round(float(np.percentile(e, 10)) * 1e3, 3),
-                         "us_p90": round(float(np.percentile(e, 90)) * 1e3, 3),
-                         "kernel": L.qkn_last_launch()["kernel"],
-                         "grid": L.qkn_last_launch()["grid"]}
+            us = time_graph(torch, lambda i, c=dcase: c.launch(0), 200, 10) * 1e3
+            lat[name] = {"us_per_launch_graph": round(us, 3), "kernel": L.qkn_last_launch()["kernel"],
+                         "grid": L.qkn_last_launch()["grid"], "bytes": dcase.bytes}
             del dcase
         extras["decode_latency_warm"] = lat
         # long prefill shard
-        lwl = workloads.LONG_PREFILL_TP4
-        lcase = Case(lwl, 0, min_fp, torch, L, workloads)
-        r, e = time_launches(torch, lcase.launch, max(20, args.steps // 4), 5)
-        lk = float(np.mean(e))
+        lcase = Case(workloads.LONG_PREFILL_TP4, 0, min_fp, torch, L, workloads)
+        nl = max(20, args.steps // 4)
+        lk = time_region(torch, lcase.launch, nl, 5) / nl
         extras["long_prefill_tp4"] = {"kernel": L.qkn_last_launch()["kernel"], "bytes": lcase.bytes,
                                       "kernel_us": round(lk * 1e3, 3),
                                       "gbs": round(lcase.bytes / (lk * 1e-3) / 1e9, 1)}
         del lcase
-        print(f"[bench] extras done", file=sys.stderr, flush=True)
+        print("[bench] extras done", file=sys.stderr, flush=True)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -284,8 +427,10 @@ def main():
                    "kernel": info["kernel"], "grid": info["grid"], "block": info["block"],
                    "parallelism": "1 GPU (peer ranks simulated)"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel_us": round(kernel_ms * 1e3, 3)},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_bytes(info["kernel"], wl.name),
+                     "algorithmic_bytes": case.bytes, "kernel_us": round(kernel_ms * 1e3, 3),
+                     "isolated_launch_us": round(isolated_ms * 1e3, 3)},
         "cpu_baseline": cpu,
         "extras": extras,
     }

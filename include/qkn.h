@@ -157,8 +157,15 @@ int qkn_last_launch(qkn_launch_info* info);
 /*
  * Process-wide tuning knobs (for benchmarks and tests; not thread-safe with
  * concurrent launches). Keys:
- *   "waves_per_cu"   cap on resident wavefronts per CU used to size the
- *                    persistent grid (0 = occupancy limit, the default);
+ *   "waves_per_cu"   wavefronts per CU used to size the grid (0 = the
+ *                    default: enough to keep ~24 KB of rows requested per
+ *                    CU, at least 6, at most the occupancy limit; larger
+ *                    values oversubscribe, which is correct but not
+ *                    persistent);
+ *   "prefetch"       1 = pipelined kernels that request the next token
+ *                    before writing the current one, 0 = not (default);
+ *   "token_blocks"   1 = each wavefront takes a contiguous range of tokens,
+ *                    0 = tokens strided by the wavefront count (default);
  *   "waves_per_block" 1..4, 0 = automatic;
  *   "force_generic"  1 = always take the general path (same results);
  *   "validate_only"  1 = entry points validate their arguments and choose a

@@ -55,6 +55,10 @@ constexpr int kChunk = 8;           // bf16 elements per 128-bit access
 constexpr int kMaxRegChunks = 8;    // chunks per lane held in registers (d_local <= 4096)
 constexpr int kMaxFastTp = kWave;   // one statistic slot per lane
 constexpr int kMaxStageBytes = 64 * 1024;
+// Grid sizing of the register path (measured on MI355X: HBM throughput peaks
+// with few, long-lived wavefronts per CU rather than full occupancy).
+constexpr int64_t kInFlightBytes = 24 * 1024;
+constexpr int64_t kMinWavesPerCu = 6;
 
 enum Mode { kFused = 0, kApply = 1, kPartial = 2 };
 
@@ -75,6 +79,7 @@ struct DevSeg {
 struct KParams {
   DevSeg seg[2];
   int64_t T;
+  int64_t tok_chunk;  // 0: wave w takes tokens w, w + W, ...; else [w*chunk, (w+1)*chunk)
   int32_t nseg;
   int32_t tp;
   int32_t rank;
@@ -179,31 +184,84 @@ __device__ __forceinline__ int64_t wave_index() {
 }
 
 // ------------------------------------------------------------------ register path
+//
+// Every memory access of the register path is a raw buffer access whose
+// descriptor covers exactly the valid bytes (built per row in scalar
+// registers; the row base is wave-uniform). Lanes whose chunk lies past the end
+// read zeros and their stores are dropped by the hardware range check, so no
+// access sits behind a branch and the compiler can count outstanding requests
+// exactly (a wait for the current token does not also wait for the next one).
+
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
+#ifndef QKN_LOAD_CPOL
+#define QKN_LOAD_CPOL 2  // non-temporal
+#endif
+#ifndef QKN_STORE_CPOL
+#define QKN_STORE_CPOL 18  // non-temporal, system scope (sc1 nt): measured best for y
+#endif
+constexpr int kLoadCpol = QKN_LOAD_CPOL;    // cache policy of the streamed x
+constexpr int kStoreCpol = QKN_STORE_CPOL;  // cache policy of the streamed y
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), kRsrcWord3);
+}
+
+// Descriptor of `bytes` bytes at base + byte offset `off`; an empty one when base is NULL.
+__device__ __forceinline__ Rsrc make_rsrc_at(const void* base, int64_t off, uint32_t bytes) {
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+  return make_rsrc(reinterpret_cast<const void*>(b ? b + off : 0), b ? bytes : 0u);
+}
+
+__device__ __forceinline__ u32x4 ld16(Rsrc r, int off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ u32x4 ld16_nt(Rsrc r, int off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadCpol));
+}
+__device__ __forceinline__ void st16_nt(u32x4 v, Rsrc r, int off) {
+  __builtin_amdgcn_raw_buffer_store_b128(
+      __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(r, 0, 0, 0)), v), r, off,
+      0, kStoreCpol);
+}
+__device__ __forceinline__ float ld4f(Rsrc r, int off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+// Lane 0 stores v at the descriptor's first word; other lanes are out of range.
+__device__ __forceinline__ void st4f_lane0(float v, Rsrc r, int lane) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, lane == 0 ? 0 : 4, 0,
+                                        0);
+}
 
 template <int N>
 __device__ __forceinline__ void load_gamma(const DevSeg& s, int lane, f32x4 (&g)[N][2]) {
+  const Rsrc r = make_rsrc(s.w, static_cast<uint32_t>(s.nchunks) * 32u);
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     const int c = i * kWave + lane;
-    if (c < s.nchunks) {
-      const f32x4* src = reinterpret_cast<const f32x4*>(s.w) + 2 * c;
-      g[i][0] = src[0];
-      g[i][1] = src[1];
-    } else {
-      g[i][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-      g[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    g[i][0] = __builtin_bit_cast(f32x4, ld16(r, c * 32));
+    g[i][1] = __builtin_bit_cast(f32x4, ld16(r, c * 32 + 16));
   }
 }
 
 template <int N>
 __device__ __forceinline__ void load_row(const DevSeg& s, int64_t t, int lane, u32x4 (&x)[N]) {
-  const u32x4* row = reinterpret_cast<const u32x4*>(s.x + t * s.ldx);
+  const Rsrc r = make_rsrc(s.x + t * s.ldx, static_cast<uint32_t>(s.nchunks) * 16u);
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
-    const int c = i * kWave + lane;
-    x[i] = (c < s.nchunks) ? __builtin_nontemporal_load(row + c) : u32x4{0u, 0u, 0u, 0u};
-  }
+  for (int i = 0; i < N; ++i) x[i] = ld16_nt(r, (i * kWave + lane) * 16);
+}
+
+// Lanes 0..tp-1 fetch rank k's statistic slot of token t (offset k*T words
+// from slot t of rank 0); the rank's own slot `skip` and lanes >= tp are out of
+// range and read 0. The register path requires tp * T * 4 < 2^31.
+__device__ __forceinline__ float load_slots_buf(const float* partials, int64_t T, int64_t t,
+                                                int lane, int tp, int skip) {
+  const uint32_t nrec = static_cast<uint32_t>((tp - 1) * T * 4 + 4);
+  const Rsrc r = make_rsrc_at(partials, t * 4, nrec);
+  const int off = (lane < tp && lane != skip) ? static_cast<int>(lane * T * 4)
+                                              : static_cast<int>(nrec);
+  return ld4f(r, off);
 }
 
 template <int N>
@@ -233,95 +291,150 @@ __device__ __forceinline__ void times_gamma(const u32x4 (&x)[N], const f32x4 (&g
 template <int N>
 __device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t t, int lane,
                                              const float (&z)[N][8], float inv) {
-  u32x4* row = reinterpret_cast<u32x4*>(s.y + t * s.ldy);
+  const Rsrc r = make_rsrc(s.y + t * s.ldy, static_cast<uint32_t>(s.nchunks) * 16u);
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    const int c = i * kWave + lane;
-    if (c < s.nchunks) {
-      u32x4 o;
+    u32x4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(z[i][2 * e] * inv, z[i][2 * e + 1] * inv);
-      __builtin_nontemporal_store(o, row + c);
-    }
+    for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(z[i][2 * e] * inv, z[i][2 * e + 1] * inv);
+    st16_nt(o, r, (i * kWave + lane) * 16);
   }
 }
 
+// Registers of one token in flight: its Q and K chunks and its statistic slots.
+template <int N0, int M1>
+struct TokenRegs {
+  u32x4 x0[N0];
+  u32x4 x1[M1];
+  float slots0;
+  float slots1;
+};
+
 template <int N0, int N1, int MODE>
+__device__ __forceinline__ void fetch_token(const KParams& p, int64_t t, int lane, int own_rank,
+                                            TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r) {
+  load_row<N0>(p.seg[0], t, lane, r.x0);
+  if constexpr (N1 > 0) load_row<N1>(p.seg[1], t, lane, r.x1);
+  r.slots0 = 0.0f;
+  r.slots1 = 0.0f;
+  if constexpr (MODE != kPartial) {
+    // with tp == 1 (fused) every lane is out of range: nothing is read
+    r.slots0 = load_slots_buf(p.seg[0].partials, p.T, t, lane, p.tp, own_rank);
+    if constexpr (N1 > 0) r.slots1 = load_slots_buf(p.seg[1].partials, p.T, t, lane, p.tp, own_rank);
+  }
+}
+
+// Phases A, B and C of token t, whose rows and slots are in `r`.
+template <int N0, int N1, int MODE>
+__device__ __forceinline__ void process_token(const KParams& p, int64_t t, int lane,
+                                              int own_rank, const f32x4 (&g0)[N0][2],
+                                              const f32x4 (&g1)[(N1 > 0 ? N1 : 1)][2],
+                                              const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r) {
+  constexpr int M1 = N1 > 0 ? N1 : 1;
+  const DevSeg& s0 = p.seg[0];
+  const DevSeg& s1 = p.seg[1];
+
+  // Phase A: per-lane partial sums (not needed when every slot is given).
+  float a0 = 0.0f, a1 = 0.0f;
+  if constexpr (MODE != kApply) {
+    a0 = row_lane_sumsq<N0>(r.x0);
+    if constexpr (N1 > 0) a1 = row_lane_sumsq<N1>(r.x1);
+  }
+
+  if constexpr (MODE == kPartial) {
+    const float own0 = wave_sum(a0);
+    st4f_lane0(own0, make_rsrc_at(s0.partials, t * 4, 4u), lane);
+  } else {
+    // Phase B, compute path: independent of the statistic.
+    float z0[N0][8];
+    float z1[M1][8];
+    times_gamma<N0>(r.x0, g0, z0);
+    if constexpr (N1 > 0) times_gamma<N1>(r.x1, g1, z1);
+
+    // Phase B, reduction path.
+    float own0 = 0.0f, own1 = 0.0f;
+    if constexpr (MODE == kFused) {
+      own0 = wave_sum(a0);
+      if constexpr (N1 > 0) own1 = wave_sum(a1);
+    }
+    const float S0 = combine_slots(r.slots0, own0, p.tp, own_rank);
+    const float inv0 = rms_inverse(S0, s0.d_full, p.eps);
+    float inv1 = 0.0f;
+    if constexpr (N1 > 0) {
+      const float S1 = combine_slots(r.slots1, own1, p.tp, own_rank);
+      inv1 = rms_inverse(S1, s1.d_full, p.eps);
+    }
+
+    // Phase C.
+    store_scaled<N0>(s0, t, lane, z0, inv0);
+    if constexpr (N1 > 0) store_scaled<N1>(s1, t, lane, z1, inv1);
+    const int64_t own_slot = (static_cast<int64_t>(p.rank) * p.T + t) * 4;
+    if constexpr (MODE == kFused) {
+      st4f_lane0(own0, make_rsrc_at(s0.partials, own_slot, 4u), lane);
+      if constexpr (N1 > 0) st4f_lane0(own1, make_rsrc_at(s1.partials, own_slot, 4u), lane);
+    }
+    st4f_lane0(inv0, make_rsrc_at(s0.inv_rms, t * 4, 4u), lane);
+    if constexpr (N1 > 0) st4f_lane0(inv1, make_rsrc_at(s1.inv_rms, t * 4, 4u), lane);
+  }
+}
+
+// Persistent register-resident kernel. N0/N1: 16-byte chunks per lane of the
+// two segments (N1 = 0: one segment). PF: software pipelining -- the next
+// token's rows and slots are requested before the current token is reduced
+// and written, so each wavefront keeps two tokens in flight. Two register sets
+// alternate roles (the loop is unrolled by two) so that no copy forces a wait
+// on the requests in flight; the next-token index is clamped to the last token
+// so every request is unconditional.
+template <int N0, int N1, int MODE, bool PF>
 __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
   constexpr int M1 = N1 > 0 ? N1 : 1;
   const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
   const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (blockDim.x / kWave);
-  const DevSeg& s0 = p.seg[0];
-  const DevSeg& s1 = p.seg[1];
   const int own_rank = (MODE == kFused) ? p.rank : -1;
+
+  const int64_t w = wave_index();
+  int64_t t, step, end;
+  if (p.tok_chunk > 0) {
+    t = w * p.tok_chunk;
+    step = 1;
+    end = (t + p.tok_chunk < p.T) ? t + p.tok_chunk : p.T;
+  } else {
+    t = w;
+    step = nwaves;
+    end = p.T;
+  }
+  if (t >= end) return;
 
   f32x4 g0[N0][2];
   f32x4 g1[M1][2];
   if constexpr (MODE != kPartial) {
-    load_gamma<N0>(s0, lane, g0);
-    if constexpr (N1 > 0) load_gamma<N1>(s1, lane, g1);
+    load_gamma<N0>(p.seg[0], lane, g0);
+    if constexpr (N1 > 0) load_gamma<N1>(p.seg[1], lane, g1);
   }
 
-  for (int64_t t = wave_index(); t < p.T; t += nwaves) {
-    u32x4 x0[N0];
-    u32x4 x1[M1];
-    load_row<N0>(s0, t, lane, x0);
-    if constexpr (N1 > 0) load_row<N1>(s1, t, lane, x1);
-
-    float slots0 = 0.0f, slots1 = 0.0f;
-    if constexpr (MODE != kPartial) {
-      if (p.tp > 1 || MODE == kApply) {
-        slots0 = load_slots(s0.partials, p.T, t, lane, p.tp, own_rank);
-        if constexpr (N1 > 0) slots1 = load_slots(s1.partials, p.T, t, lane, p.tp, own_rank);
-      }
+  TokenRegs<N0, M1> ra;
+  fetch_token<N0, N1, MODE>(p, t, lane, own_rank, ra);
+  if constexpr (PF) {
+    TokenRegs<N0, M1> rb;
+    const int64_t last = end - 1;
+    while (true) {
+      int64_t tn = t + step;
+      fetch_token<N0, N1, MODE>(p, tn < last ? tn : last, lane, own_rank, rb);
+      process_token<N0, N1, MODE>(p, t, lane, own_rank, g0, g1, ra);
+      if (tn > last) break;
+      t = tn;
+      tn = t + step;
+      fetch_token<N0, N1, MODE>(p, tn < last ? tn : last, lane, own_rank, ra);
+      process_token<N0, N1, MODE>(p, t, lane, own_rank, g0, g1, rb);
+      if (tn > last) break;
+      t = tn;
     }
-
-    // Phase A: per-lane partial sums (not needed when every slot is given).
-    float a0 = 0.0f, a1 = 0.0f;
-    if constexpr (MODE != kApply) {
-      a0 = row_lane_sumsq<N0>(x0);
-      if constexpr (N1 > 0) a1 = row_lane_sumsq<N1>(x1);
-    }
-
-    if constexpr (MODE == kPartial) {
-      const float own0 = wave_sum(a0);
-      if (lane == 0) s0.partials[t] = own0;
-    } else {
-      // Phase B, compute path: independent of the statistic.
-      float z0[N0][8];
-      float z1[M1][8];
-      times_gamma<N0>(x0, g0, z0);
-      if constexpr (N1 > 0) times_gamma<N1>(x1, g1, z1);
-
-      // Phase B, reduction path.
-      float own0 = 0.0f, own1 = 0.0f;
-      if constexpr (MODE == kFused) {
-        own0 = wave_sum(a0);
-        if constexpr (N1 > 0) own1 = wave_sum(a1);
-      }
-      const float S0 = combine_slots(slots0, own0, p.tp, own_rank);
-      const float inv0 = rms_inverse(S0, s0.d_full, p.eps);
-      float inv1 = 0.0f;
-      if constexpr (N1 > 0) {
-        const float S1 = combine_slots(slots1, own1, p.tp, own_rank);
-        inv1 = rms_inverse(S1, s1.d_full, p.eps);
-      }
-
-      // Phase C.
-      store_scaled<N0>(s0, t, lane, z0, inv0);
-      if constexpr (N1 > 0) store_scaled<N1>(s1, t, lane, z1, inv1);
-      if (lane == 0) {
-        if constexpr (MODE == kFused) {
-          if (s0.partials) s0.partials[static_cast<int64_t>(p.rank) * p.T + t] = own0;
-          if constexpr (N1 > 0) {
-            if (s1.partials) s1.partials[static_cast<int64_t>(p.rank) * p.T + t] = own1;
-          }
-        }
-        if (s0.inv_rms) s0.inv_rms[t] = inv0;
-        if constexpr (N1 > 0) {
-          if (s1.inv_rms) s1.inv_rms[t] = inv1;
-        }
-      }
+  } else {
+    while (true) {
+      process_token<N0, N1, MODE>(p, t, lane, own_rank, g0, g1, ra);
+      t += step;
+      if (t >= end) break;
+      fetch_token<N0, N1, MODE>(p, t, lane, own_rank, ra);
     }
   }
 }
@@ -429,34 +542,38 @@ typedef void (*GenericFn)(KParams, int32_t);
 constexpr int kNIdx[9] = {-1, 0, 1, 2, 2, 3, 3, 3, 3};  // chunks/lane -> table index
 constexpr int kNVal[4] = {1, 2, 4, 8};
 
-#define QKN_ROW_SET(M, A)                                                              \
-  {qkn_rows<A, 0, M>, qkn_rows<A, 1, M>, qkn_rows<A, 2, M>, qkn_rows<A, 4, M>,         \
-   qkn_rows<A, 8, M>}
+#define QKN_ROW_SET(M, A, PF)                                                          \
+  {qkn_rows<A, 0, M, PF>, qkn_rows<A, 1, M, PF>, qkn_rows<A, 2, M, PF>,                 \
+   qkn_rows<A, 4, M, PF>, qkn_rows<A, 8, M, PF>}
+#define QKN_ONE_SET(M, PF) \
+  {qkn_rows<1, 0, M, PF>, qkn_rows<2, 0, M, PF>, qkn_rows<4, 0, M, PF>, qkn_rows<8, 0, M, PF>}
 
-// [N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
-const RowsFn kFusedTable[4][5] = {QKN_ROW_SET(kFused, 1), QKN_ROW_SET(kFused, 2),
-                                  QKN_ROW_SET(kFused, 4), QKN_ROW_SET(kFused, 8)};
-const RowsFn kApplyTable[4] = {qkn_rows<1, 0, kApply>, qkn_rows<2, 0, kApply>,
-                               qkn_rows<4, 0, kApply>, qkn_rows<8, 0, kApply>};
-const RowsFn kPartialTable[4] = {qkn_rows<1, 0, kPartial>, qkn_rows<2, 0, kPartial>,
-                                 qkn_rows<4, 0, kPartial>, qkn_rows<8, 0, kPartial>};
+// [prefetch][N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
+const RowsFn kFusedTable[2][4][5] = {
+    {QKN_ROW_SET(kFused, 1, false), QKN_ROW_SET(kFused, 2, false), QKN_ROW_SET(kFused, 4, false),
+     QKN_ROW_SET(kFused, 8, false)},
+    {QKN_ROW_SET(kFused, 1, true), QKN_ROW_SET(kFused, 2, true), QKN_ROW_SET(kFused, 4, true),
+     QKN_ROW_SET(kFused, 8, true)}};
+const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(kApply, false), QKN_ONE_SET(kApply, true)};
+const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(kPartial, false), QKN_ONE_SET(kPartial, true)};
 const GenericFn kGenericTable[3] = {qkn_generic<kFused>, qkn_generic<kApply>,
                                     qkn_generic<kPartial>};
 
 const char* const kModeName[3] = {"fused", "apply", "partial"};
 
-// Static names "rows<N0,N1>/mode" for the launch description.
-const char* rows_name(int mode, int i0, int i1) {
-  static char names[3][4][5][32];
+// Static names "rows<N0,N1>/mode" (or "rows_pf<...>" when pipelined).
+const char* rows_name(int mode, int pf, int i0, int i1) {
+  static char names[3][2][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
     for (int m = 0; m < 3; ++m)
-      for (int a = 0; a < 4; ++a)
-        for (int b = 0; b < 5; ++b)
-          snprintf(names[m][a][b], sizeof(names[m][a][b]), "rows<%d,%d>/%s", kNVal[a],
-                   b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
+      for (int f = 0; f < 2; ++f)
+        for (int a = 0; a < 4; ++a)
+          for (int b = 0; b < 5; ++b)
+            snprintf(names[m][f][a][b], sizeof(names[m][f][a][b]), "%s<%d,%d>/%s",
+                     f ? "rows_pf" : "rows", kNVal[a], b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
   });
-  return names[mode][i0][i1];
+  return names[mode][pf][i0][i1];
 }
 const char* const kGenericName[3] = {"generic/fused", "generic/apply", "generic/partial"};
 
@@ -465,6 +582,8 @@ int64_t g_opt_waves_per_cu = 0;
 int64_t g_opt_waves_per_block = 0;
 int64_t g_opt_force_generic = 0;
 int64_t g_opt_validate_only = 0;
+int64_t g_opt_prefetch = 0;
+int64_t g_opt_token_blocks = 0;
 
 thread_local qkn_launch_info t_last = {nullptr, 0, 0, 0, 0};
 
@@ -657,7 +776,8 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   kp.tp = tp;
   kp.rank = rank;
   kp.eps = eps;
-  bool fast = (g_opt_force_generic == 0) && tp <= kMaxFastTp;
+  bool fast = (g_opt_force_generic == 0) && tp <= kMaxFastTp &&
+              static_cast<__int128>(tp) * T * 4 < (static_cast<__int128>(1) << 31);
   int idx[2] = {0, 0};
   int max_chunks = 0;
   for (int i = 0; i < nseg; ++i) {
@@ -673,10 +793,11 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   int lds = 0;
   int32_t stage_elems = 0;
   if (fast) {
-    if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
-    else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[idx[0]]);
-    else fn = reinterpret_cast<const void*>(kPartialTable[idx[0]]);
-    name = rows_name(mode, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+    const int pf = g_opt_prefetch ? 1 : 0;
+    if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[pf][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
+    else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[pf][idx[0]]);
+    else fn = reinterpret_cast<const void*>(kPartialTable[pf][idx[0]]);
+    name = rows_name(mode, pf, idx[0], nseg == 2 ? idx[1] + 1 : 0);
   } else {
     fn = reinterpret_cast<const void*>(kGenericTable[mode]);
     name = kGenericName[mode];
@@ -694,21 +815,28 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   int rc = query_device(&dev, &cus);
   if (rc != QKN_OK) return rc;
   int wpb = 1;
-  if (fast) {
-    if (g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
-    else wpb = (T <= 4 * static_cast<int64_t>(cus)) ? 1 : 4;
-  }
+  if (fast && g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
   const int block = wpb * kWave;
   int bpc = 0;
   rc = blocks_per_cu(dev, fn, block, lds, &bpc);
   if (rc != QKN_OK) return rc;
+  // Persistent grid: enough wavefronts per CU to keep about kInFlightBytes of
+  // rows requested per CU, at least kMinWavesPerCu, at most what fits.
   int64_t waves_per_cu = static_cast<int64_t>(bpc) * wpb;
-  if (g_opt_waves_per_cu > 0 && g_opt_waves_per_cu < waves_per_cu) waves_per_cu = g_opt_waves_per_cu;
+  if (fast) {
+    int64_t token_bytes = 0;
+    for (int i = 0; i < nseg; ++i) token_bytes += 2 * static_cast<int64_t>(kp.seg[i].d);
+    int64_t want = (kInFlightBytes + token_bytes - 1) / token_bytes;
+    if (want < kMinWavesPerCu) want = kMinWavesPerCu;
+    if (want < waves_per_cu) waves_per_cu = want;
+  }
+  if (g_opt_waves_per_cu > 0) waves_per_cu = g_opt_waves_per_cu;
   if (waves_per_cu < 1) waves_per_cu = 1;
   int64_t waves = waves_per_cu * cus;
   if (waves > T) waves = T;
   int64_t grid = (waves + wpb - 1) / wpb;
   if (grid > 0x7fffffff) grid = 0x7fffffff;
+  if (fast && g_opt_token_blocks) kp.tok_chunk = (T + grid * wpb - 1) / (grid * wpb);
 
   hipError_t err;
   if (fast) {
@@ -837,6 +965,12 @@ int qkn_set_option(const char* key, int64_t value) {
   } else if (strcmp(key, "force_generic") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_force_generic = value;
+  } else if (strcmp(key, "prefetch") == 0) {
+    if (value != 0 && value != 1) return QKN_EINVAL;
+    g_opt_prefetch = value;
+  } else if (strcmp(key, "token_blocks") == 0) {
+    if (value != 0 && value != 1) return QKN_EINVAL;
+    g_opt_token_blocks = value;
   } else if (strcmp(key, "validate_only") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_validate_only = value;

@@ -29,8 +29,8 @@ def lib():
 def dry(lib):
     assert lib.qkn_set_option(b"validate_only", 1) == 0
     yield lib
-    assert lib.qkn_set_option(b"validate_only", 0) == 0
-    assert lib.qkn_set_option(b"force_generic", 0) == 0
+    for key in (b"validate_only", b"force_generic", b"prefetch", b"token_blocks"):
+        assert lib.qkn_set_option(key, 0) == 0
 
 
 def _declared_functions():
@@ -76,27 +76,49 @@ def _k(T=64, d=256, rank_tp=4):
 def test_valid_calls_pass_validation(dry):
     assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
     info = L.qkn_last_launch()
-    assert info["kernel"] == "rows<2,1>/fused" and info["grid"] == 0
+    assert info["kernel"].endswith("<2,1>/fused") and info["grid"] == 0
     assert dry.qkn_partial_sumsq(BASE, 1024, 64, 1024, BASE + 64 * MB, None) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/partial"
+    assert L.qkn_last_launch()["kernel"].endswith("<2,0>/partial")
     assert dry.qkn_apply(BASE, 1024, BASE + 64 * MB, BASE + 65 * MB, 4, 64, 1024, 4096,
                          ctypes.c_float(1e-6), BASE + 128 * MB, 1024, None, None) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/apply"
+    assert L.qkn_last_launch()["kernel"].endswith("<2,0>/apply")
     full = [_seg(BASE, 4096, BASE + 64 * MB, 0, BASE + 128 * MB, 4096, 4096, 4096),
             _seg(BASE + 256 * MB, 1024, BASE + 300 * MB, 0, BASE + 400 * MB, 1024, 1024, 1024)]
     arr = (L.QknSeg * 2)(*full)
     assert dry.qkn_full(arr, 2, 8192, ctypes.c_float(1e-6), None) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows<8,2>/fused"
+    assert L.qkn_last_launch()["kernel"].endswith("<8,2>/fused")
 
 
-@pytest.mark.parametrize("d,expect", [(8, "rows<1,0>"), (512, "rows<1,0>"), (520, "rows<2,0>"),
-                                      (2048, "rows<4,0>"), (1536, "rows<4,0>"),
-                                      (4096, "rows<8,0>"), (4104, "generic"),
+@pytest.mark.parametrize("d,expect", [(8, "<1,0>"), (512, "<1,0>"), (520, "<2,0>"),
+                                      (2048, "<4,0>"), (1536, "<4,0>"),
+                                      (4096, "<8,0>"), (4104, "generic"),
                                       (100, "generic"), (1, "generic")])
 def test_path_choice_by_width(dry, d, expect):
     seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
     assert _fused(dry, [seg], 2, 0, 16) == 0
-    assert L.qkn_last_launch()["kernel"].startswith(expect)
+    name = L.qkn_last_launch()["kernel"]
+    assert name.startswith("generic") if expect == "generic" else (name.startswith("rows") and expect in name)
+
+
+def test_prefetch_option_selects_variant(dry):
+    seg = _seg(BASE, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 2048)
+    assert dry.qkn_set_option(b"prefetch", 0) == 0
+    assert _fused(dry, [seg], 2, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/fused"
+    assert dry.qkn_set_option(b"prefetch", 1) == 0
+    assert _fused(dry, [seg], 2, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_pf<2,0>/fused"
+    assert dry.qkn_set_option(b"prefetch", 2) == L.QKN_EINVAL
+
+
+def test_register_path_needs_slot_offsets_in_range(dry):
+    # tp * T * 4 bytes of statistics must stay below 2^31 for the register path
+    G = 1 << 34  # regions of 16 GiB apart: x and y of 8M tokens x 1024 bf16 fit
+    seg = _seg(BASE, 1024, BASE + 3 * G, BASE + 2 * G, BASE + G, 1024, 1024, 64 * 1024)
+    assert _fused(dry, [seg], 64, 0, (1 << 31) // (64 * 4)) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    assert _fused(dry, [seg], 64, 0, (1 << 31) // (64 * 4) - 1) == 0
+    assert L.qkn_last_launch()["kernel"].startswith("rows")
 
 
 def test_path_choice_alignment_and_options(dry):
