@@ -56,6 +56,7 @@ extern "C" {
 #define QKN_EINVAL (-1)   /* bad argument: NULL required pointer, bad size, tp/rank, eps */
 #define QKN_EOVERLAP (-2) /* an output overlaps an input or another output in part */
 #define QKN_EHIP (-3)     /* the HIP runtime refused a query or a launch */
+#define QKN_ENOTSUP (-4)  /* shape/alignment outside what this entry point supports */
 
 /*
  * One tensor (Q or K) of one rank.
@@ -134,6 +135,74 @@ int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, 
  * may be NULL (else it receives the full sum of squares per token).
  */
 int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream);
+
+/*
+ * Published statistics, for ranks that run concurrently (Sec. III-B; Alg. 1
+ * Phase B, where each GPU signals its peers and spins on a local flag).
+ * A slot is one 8-byte word: the fp32 statistic's bits in the low half and the
+ * round's epoch in the high half, written by one aligned 64-bit store, so a
+ * reader that sees the epoch also sees the value. Slot arrays are uint64
+ * [tp * T], rank-major (slot k*T + t), one per tensor; they need no reset
+ * between rounds: each round uses a new nonzero epoch.
+ */
+
+/*
+ * Phase A of one rank's slice, published: slots_out[t] = {sum_j x[t, j]^2,
+ * epoch} (the same fp32 value as qkn_partial_sumsq). slots_out is uint64 [T]
+ * (point it at rank k's part, slots + k*T, of a slot array), 8-byte aligned.
+ * Register path only: QKN_ENOTSUP unless x is 16-byte aligned, ldx and
+ * d_local are multiples of 8 and d_local <= 4096. QKN_EINVAL: NULL pointers
+ * with T > 0, epoch 0, misaligned slots_out, T < 0, d_local < 1,
+ * ldx < d_local. QKN_EOVERLAP: slots_out overlaps x.
+ */
+int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                         uint64_t* slots_out, uint32_t epoch, void* stream);
+
+typedef struct qkn_wait {
+  uint64_t* slots[2];  /* per segment: slot array [tp * T] (see above) */
+  uint32_t epoch;      /* nonzero: the slots of this round carry it */
+  int64_t spin_limit;  /* polls of one slot before giving up (>= 1) */
+  int co_resident;     /* kernels on this GPU that wait on each other (>= 1): the
+                          grid is sized so that all of their wavefronts are
+                          resident together (Sec. III-D's bound) */
+  int32_t* status;     /* device int, set to 1 if any wait gave up; the caller
+                          clears it. Outputs of tokens that gave up are NaN. */
+} qkn_wait;
+
+/*
+ * qkn_fused_shard for ranks that run concurrently: per token and tensor the
+ * kernel publishes its own statistic to slots[i][rank*T + t], forms x * w,
+ * and then waits (lanes 0..tp-1, one peer each) until every other rank's slot
+ * of that token carries `epoch`, before combining them in ascending rank order
+ * (Alg. 1). Results are bit-identical to qkn_fused_shard given the same
+ * statistics. A wait that exceeds spin_limit polls sets *status = 1 and the
+ * wavefront stops waiting for its later tokens; every kernel exits normally.
+ * segs[i].partials must be NULL (statistics travel in the slots).
+ * QKN_EINVAL: as qkn_fused_shard, and wait NULL, epoch 0, spin_limit < 1,
+ * co_resident < 1, a NULL or misaligned slot array or status, partials set.
+ * QKN_ENOTSUP: a segment outside the register path (see qkn_publish_partials).
+ * QKN_EOVERLAP: slot arrays or status overlapping anything else.
+ */
+int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
+                         const qkn_wait* wait, void* stream);
+
+/*
+ * Every rank of a tp group in one launch (ranks that share one GPU, or a
+ * single-GPU rehearsal of the exchange): segs describe the FULL tensors --
+ * x, y bf16 [T, ld >= d_full], w fp32 [d_full] -- with d_local the slice width
+ * and d_full == tp * d_local; rank r's slice is columns [r*d_local,
+ * (r+1)*d_local). Wavefront w computes rank w mod tp: it publishes that rank's
+ * statistic to slots[i][r*T + t] and waits for the other ranks' as in
+ * qkn_fused_shard_wait. Because all ranks are in one launch whose grid fits
+ * on the GPU at once, every wavefront a wait depends on is resident (the
+ * bound of Sec. III-D), which separate kernels on separate streams do not
+ * guarantee on one GPU. inv_rms, if not NULL, is fp32 [tp * T] (rank-major;
+ * every rank's factors are equal). The output y is the unsharded QK-Norm.
+ * QKN_EINVAL/QKN_ENOTSUP/QKN_EOVERLAP as qkn_fused_shard_wait, and
+ * d_full != tp * d_local or ld < d_full.
+ */
+int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float eps,
+                         const qkn_wait* wait, void* stream);
 
 /* Static text for a status code (never NULL). */
 const char* qkn_strerror(int status);

@@ -21,7 +21,7 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqkn.so")
 
-QKN_OK, QKN_EINVAL, QKN_EOVERLAP, QKN_EHIP = 0, -1, -2, -3
+QKN_OK, QKN_EINVAL, QKN_EOVERLAP, QKN_EHIP, QKN_ENOTSUP = 0, -1, -2, -3, -4
 
 _c_i64 = ctypes.c_int64
 _vp = ctypes.c_void_p
@@ -31,6 +31,11 @@ class QknSeg(ctypes.Structure):
     _fields_ = [("x", _vp), ("ldx", _c_i64), ("w", _vp), ("partials", _vp),
                 ("y", _vp), ("ldy", _c_i64), ("inv_rms", _vp),
                 ("d_local", _c_i64), ("d_full", _c_i64)]
+
+
+class QknWait(ctypes.Structure):
+    _fields_ = [("slots", _vp * 2), ("epoch", ctypes.c_uint32), ("spin_limit", _c_i64),
+                ("co_resident", ctypes.c_int), ("status", _vp)]
 
 
 class QknLaunchInfo(ctypes.Structure):
@@ -62,12 +67,19 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qkn_fused_shard.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, _c_i64, ctypes.c_float, _vp]
     lib.qkn_full.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, _c_i64, ctypes.c_float, _vp]
+    lib.qkn_publish_partials.argtypes = [_vp, _c_i64, _c_i64, _c_i64, _vp, ctypes.c_uint32, _vp]
+    lib.qkn_fused_shard_wait.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, ctypes.c_int,
+                                         ctypes.c_int, _c_i64, ctypes.c_float,
+                                         ctypes.POINTER(QknWait), _vp]
+    lib.qkn_fused_group_wait.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, ctypes.c_int,
+                                         _c_i64, ctypes.c_float, ctypes.POINTER(QknWait), _vp]
     lib.qkn_strerror.argtypes = [ctypes.c_int]
     lib.qkn_strerror.restype = ctypes.c_char_p
     lib.qkn_last_launch.argtypes = [ctypes.POINTER(QknLaunchInfo)]
     lib.qkn_set_option.argtypes = [ctypes.c_char_p, _c_i64]
     for name in ("qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
-                 "qkn_last_launch", "qkn_set_option"):
+                 "qkn_last_launch", "qkn_set_option", "qkn_publish_partials",
+                 "qkn_fused_shard_wait", "qkn_fused_group_wait"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -192,6 +204,75 @@ def qkn_full(segs: Sequence[Seg], eps: float, stream=None):
     """TP = 1 full-vector QK-Norm (d_full == d_local for every segment)."""
     arr, T = _segs(segs, 1)
     _check(load().qkn_full(arr, len(segs), T, eps, _stream(stream)), "qkn_full")
+    return [s.y for s in segs]
+
+
+def _slots(t: torch.Tensor, numel: int, what: str) -> int:
+    """Flagged-slot array: a contiguous int64 GPU tensor (8-byte words)."""
+    if t.dtype != torch.int64 or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{what}: expected a contiguous int64 GPU tensor of 8-byte slots")
+    if t.numel() < numel:
+        raise ValueError(f"{what}: needs {numel} slots, has {t.numel()}")
+    return t.data_ptr()
+
+
+def qkn_publish_partials(x: torch.Tensor, slots_out: torch.Tensor, epoch: int,
+                         stream=None) -> None:
+    """Phase A of x [T, d_local], published as flagged slots (int64 [T], one per token)."""
+    px, ldx, T, d = _rows(x, "x")
+    _check(load().qkn_publish_partials(px, ldx, T, d, _slots(slots_out, T, "slots_out"),
+                                       epoch, _stream(stream)), "qkn_publish_partials")
+
+
+def make_wait(slots: Sequence[torch.Tensor], tp: int, T: int, epoch: int, spin_limit: int,
+              co_resident: int, status: torch.Tensor) -> QknWait:
+    """The qkn_wait block: slots are int64 [tp, T] per segment, status int32 [>= 1]."""
+    if status.dtype != torch.int32 or not status.is_cuda or status.numel() < 1:
+        raise ValueError("status: expected an int32 GPU tensor")
+    ptrs = [_slots(sl, tp * T, f"slots[{i}]") for i, sl in enumerate(slots)] + [None]
+    return QknWait((_vp * 2)(ptrs[0], ptrs[1] if len(slots) > 1 else None), epoch, spin_limit,
+                   co_resident, status.data_ptr())
+
+
+def qkn_fused_shard_wait(segs: Sequence[Seg], tp: int, rank: int, eps: float,
+                         slots: Sequence[torch.Tensor], epoch: int, spin_limit: int,
+                         co_resident: int, status: torch.Tensor, stream=None):
+    """Fused QK-Norm that publishes its statistics and waits for the other ranks'."""
+    arr, T = _segs(segs, tp)
+    wait = make_wait(slots, tp, T, epoch, spin_limit, co_resident, status)
+    _check(load().qkn_fused_shard_wait(arr, len(segs), tp, rank, T, eps, ctypes.byref(wait),
+                                       _stream(stream)), "qkn_fused_shard_wait")
+    return [s.y for s in segs]
+
+
+def qkn_fused_group_wait(segs: Sequence[Seg], tp: int, eps: float,
+                         slots: Sequence[torch.Tensor], epoch: int, spin_limit: int,
+                         status: torch.Tensor, stream=None):
+    """Every rank of a tp group in one launch over the full tensors.
+
+    segs[i].x / .y are the full bf16 [T, d_full] tensors, .w the full gamma,
+    .d_full the full width; each rank's slice is d_full / tp columns. inv_rms,
+    if given, is fp32 [tp, T].
+    """
+    arr = (QknSeg * len(segs))()
+    T = None
+    for i, s in enumerate(segs):
+        px, ldx, Ts, d_full = _rows(s.x, f"seg{i}.x")
+        if d_full != s.d_full or d_full % tp:
+            raise ValueError(f"seg{i}: x must hold the full width d_full, divisible by tp")
+        T = Ts if T is None else T
+        if Ts != T:
+            raise ValueError("all segments must have the same number of tokens")
+        if s.y is None:
+            s.y = torch.empty_like(s.x)
+        py, ldy, _, _ = _rows(s.y, f"seg{i}.y")
+        if s.partials is not None:
+            raise ValueError("statistics travel in the slots; partials must be None")
+        arr[i] = QknSeg(px, ldx, _f32(s.w, f"seg{i}.w", d_full), None, py, ldy,
+                        _f32(s.inv_rms, f"seg{i}.inv_rms", tp * Ts), d_full // tp, d_full)
+    wait = make_wait(slots, tp, T, epoch, spin_limit, 1, status)
+    _check(load().qkn_fused_group_wait(arr, len(segs), tp, T, eps, ctypes.byref(wait),
+                                       _stream(stream)), "qkn_fused_group_wait")
     return [s.y for s in segs]
 
 

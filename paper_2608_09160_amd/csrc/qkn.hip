@@ -60,7 +60,9 @@ constexpr int kMaxStageBytes = 64 * 1024;
 constexpr int64_t kInFlightBytes = 24 * 1024;
 constexpr int64_t kMinWavesPerCu = 6;
 
-enum Mode { kFused = 0, kApply = 1, kPartial = 2 };
+// kFusedWait: fused, with the other ranks' statistics published concurrently
+// as flagged slots that the kernel waits for; kPublish: Phase A into flagged slots.
+enum Mode { kFused = 0, kApply = 1, kPartial = 2, kFusedWait = 3, kPublish = 4 };
 
 struct DevSeg {
   const uint16_t* x;
@@ -78,6 +80,11 @@ struct DevSeg {
 
 struct KParams {
   DevSeg seg[2];
+  uint64_t* slots[2];  // flagged slots [tp * T] per segment (wait/publish modes)
+  int32_t* status;     // wait mode: set to 1 when a wait gives up
+  int64_t spin_limit;  // wait mode: polls per slot
+  uint32_t epoch;      // wait/publish modes: the flag of this round
+  int32_t group;       // wait mode: > 1 = every rank of the group in this launch
   int64_t T;
   int64_t tok_chunk;  // 0: wave w takes tokens w, w + W, ...; else [w*chunk, (w+1)*chunk)
   int32_t nseg;
@@ -235,8 +242,9 @@ __device__ __forceinline__ void st4f_lane0(float v, Rsrc r, int lane) {
 }
 
 template <int N>
-__device__ __forceinline__ void load_gamma(const DevSeg& s, int lane, f32x4 (&g)[N][2]) {
-  const Rsrc r = make_rsrc(s.w, static_cast<uint32_t>(s.nchunks) * 32u);
+__device__ __forceinline__ void load_gamma(const DevSeg& s, int64_t col, int lane,
+                                           f32x4 (&g)[N][2]) {
+  const Rsrc r = make_rsrc(s.w + col, static_cast<uint32_t>(s.nchunks) * 32u);
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     const int c = i * kWave + lane;
@@ -246,8 +254,9 @@ __device__ __forceinline__ void load_gamma(const DevSeg& s, int lane, f32x4 (&g)
 }
 
 template <int N>
-__device__ __forceinline__ void load_row(const DevSeg& s, int64_t t, int lane, u32x4 (&x)[N]) {
-  const Rsrc r = make_rsrc(s.x + t * s.ldx, static_cast<uint32_t>(s.nchunks) * 16u);
+__device__ __forceinline__ void load_row(const DevSeg& s, int64_t col, int64_t t, int lane,
+                                         u32x4 (&x)[N]) {
+  const Rsrc r = make_rsrc(s.x + t * s.ldx + col, static_cast<uint32_t>(s.nchunks) * 16u);
 #pragma unroll
   for (int i = 0; i < N; ++i) x[i] = ld16_nt(r, (i * kWave + lane) * 16);
 }
@@ -289,9 +298,9 @@ __device__ __forceinline__ void times_gamma(const u32x4 (&x)[N], const f32x4 (&g
 
 // Phase C: y = bf16(z * inv), non-temporal 128-bit stores.
 template <int N>
-__device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t t, int lane,
+__device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t col, int64_t t, int lane,
                                              const float (&z)[N][8], float inv) {
-  const Rsrc r = make_rsrc(s.y + t * s.ldy, static_cast<uint32_t>(s.nchunks) * 16u);
+  const Rsrc r = make_rsrc(s.y + t * s.ldy + col, static_cast<uint32_t>(s.nchunks) * 16u);
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     u32x4 o;
@@ -300,6 +309,54 @@ __device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t t, int lan
     st16_nt(o, r, (i * kWave + lane) * 16);
   }
 }
+
+// ------------------------------------------------------------------ flagged slots
+//
+// A published statistic is one 8-byte word: fp32 bits in the low half, the
+// round's epoch in the high half, written by a single aligned 64-bit store, so
+// a reader that sees the epoch also sees the value (no separate flag or fence).
+
+__device__ __forceinline__ void publish_slot(uint64_t* slot, float v, uint32_t epoch) {
+  const uint64_t word = (static_cast<uint64_t>(epoch) << 32) | __builtin_bit_cast(uint32_t, v);
+  __hip_atomic_store(slot, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Lanes 0..tp-1 other than `rank` poll rank k's slot of token t until it
+// carries `epoch`, at most `limit` times (with a short sleep between polls).
+// A lane that gives up, or any lane once `given_up` is set, returns NaN.
+__device__ __forceinline__ float wait_slot(const uint64_t* slots, int64_t T, int64_t t, int lane,
+                                           int tp, int rank, uint32_t epoch, int64_t limit,
+                                           bool given_up, bool& gave_up_now) {
+  float v = 0.0f;
+  if (lane < tp && lane != rank) {
+    v = __builtin_nanf("");
+    if (!given_up) {
+      const uint64_t* slot = slots + static_cast<int64_t>(lane) * T + t;
+      for (int64_t n = 0;;) {
+        const uint64_t word = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (static_cast<uint32_t>(word >> 32) == epoch) {
+          v = __builtin_bit_cast(float, static_cast<uint32_t>(word));
+          break;
+        }
+        if (++n >= limit) {
+          gave_up_now = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+  }
+  return v;
+}
+
+// The rank a wavefront computes and where that rank's slice sits: the launch's
+// rank with no offsets, or, when one launch runs every rank of a group, rank
+// w mod tp with its columns [rank*d_local, (rank+1)*d_local) of full tensors.
+struct WaveSlice {
+  int rank;
+  int64_t col0, col1;  // column offset of the slice in segment 0 / 1
+  int64_t inv_row;     // offset (in tokens) of this rank's factors in inv_rms
+};
 
 // Registers of one token in flight: its Q and K chunks and its statistic slots.
 template <int N0, int M1>
@@ -311,13 +368,14 @@ struct TokenRegs {
 };
 
 template <int N0, int N1, int MODE>
-__device__ __forceinline__ void fetch_token(const KParams& p, int64_t t, int lane, int own_rank,
+__device__ __forceinline__ void fetch_token(const KParams& p, const WaveSlice& ws, int64_t t,
+                                            int lane, int own_rank,
                                             TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r) {
-  load_row<N0>(p.seg[0], t, lane, r.x0);
-  if constexpr (N1 > 0) load_row<N1>(p.seg[1], t, lane, r.x1);
+  load_row<N0>(p.seg[0], ws.col0, t, lane, r.x0);
+  if constexpr (N1 > 0) load_row<N1>(p.seg[1], ws.col1, t, lane, r.x1);
   r.slots0 = 0.0f;
   r.slots1 = 0.0f;
-  if constexpr (MODE != kPartial) {
+  if constexpr (MODE == kFused || MODE == kApply) {
     // with tp == 1 (fused) every lane is out of range: nothing is read
     r.slots0 = load_slots_buf(p.seg[0].partials, p.T, t, lane, p.tp, own_rank);
     if constexpr (N1 > 0) r.slots1 = load_slots_buf(p.seg[1].partials, p.T, t, lane, p.tp, own_rank);
@@ -326,10 +384,11 @@ __device__ __forceinline__ void fetch_token(const KParams& p, int64_t t, int lan
 
 // Phases A, B and C of token t, whose rows and slots are in `r`.
 template <int N0, int N1, int MODE>
-__device__ __forceinline__ void process_token(const KParams& p, int64_t t, int lane,
-                                              int own_rank, const f32x4 (&g0)[N0][2],
+__device__ __forceinline__ void process_token(const KParams& p, const WaveSlice& ws, int64_t t,
+                                              int lane, int own_rank, const f32x4 (&g0)[N0][2],
                                               const f32x4 (&g1)[(N1 > 0 ? N1 : 1)][2],
-                                              const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r) {
+                                              const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
+                                              bool& given_up) {
   constexpr int M1 = N1 > 0 ? N1 : 1;
   const DevSeg& s0 = p.seg[0];
   const DevSeg& s1 = p.seg[1];
@@ -344,7 +403,24 @@ __device__ __forceinline__ void process_token(const KParams& p, int64_t t, int l
   if constexpr (MODE == kPartial) {
     const float own0 = wave_sum(a0);
     st4f_lane0(own0, make_rsrc_at(s0.partials, t * 4, 4u), lane);
+  } else if constexpr (MODE == kPublish) {
+    const float own0 = wave_sum(a0);
+    if (lane == 0) publish_slot(p.slots[0] + t, own0, p.epoch);
   } else {
+    float own0 = 0.0f, own1 = 0.0f;
+    if constexpr (MODE == kFused || MODE == kFusedWait) {
+      own0 = wave_sum(a0);
+      if constexpr (N1 > 0) own1 = wave_sum(a1);
+    }
+    if constexpr (MODE == kFusedWait) {
+      // publish this rank's statistics before waiting for the others'
+      if (lane == 0) {
+        publish_slot(p.slots[0] + static_cast<int64_t>(ws.rank) * p.T + t, own0, p.epoch);
+        if constexpr (N1 > 0)
+          publish_slot(p.slots[1] + static_cast<int64_t>(ws.rank) * p.T + t, own1, p.epoch);
+      }
+    }
+
     // Phase B, compute path: independent of the statistic.
     float z0[N0][8];
     float z1[M1][8];
@@ -352,29 +428,38 @@ __device__ __forceinline__ void process_token(const KParams& p, int64_t t, int l
     if constexpr (N1 > 0) times_gamma<N1>(r.x1, g1, z1);
 
     // Phase B, reduction path.
-    float own0 = 0.0f, own1 = 0.0f;
-    if constexpr (MODE == kFused) {
-      own0 = wave_sum(a0);
-      if constexpr (N1 > 0) own1 = wave_sum(a1);
+    float slots0 = r.slots0, slots1 = r.slots1;
+    if constexpr (MODE == kFusedWait) {
+      bool gave_up = false;
+      slots0 = wait_slot(p.slots[0], p.T, t, lane, p.tp, ws.rank, p.epoch, p.spin_limit, given_up,
+                         gave_up);
+      if constexpr (N1 > 0)
+        slots1 = wait_slot(p.slots[1], p.T, t, lane, p.tp, ws.rank, p.epoch, p.spin_limit,
+                           given_up || gave_up, gave_up);
+      if (__ballot(gave_up) != 0) {
+        if (!given_up && lane == 0)
+          __hip_atomic_store(p.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        given_up = true;  // later tokens of this wavefront do not wait again
+      }
     }
-    const float S0 = combine_slots(r.slots0, own0, p.tp, own_rank);
+    const float S0 = combine_slots(slots0, own0, p.tp, own_rank);
     const float inv0 = rms_inverse(S0, s0.d_full, p.eps);
     float inv1 = 0.0f;
     if constexpr (N1 > 0) {
-      const float S1 = combine_slots(r.slots1, own1, p.tp, own_rank);
+      const float S1 = combine_slots(slots1, own1, p.tp, own_rank);
       inv1 = rms_inverse(S1, s1.d_full, p.eps);
     }
 
     // Phase C.
-    store_scaled<N0>(s0, t, lane, z0, inv0);
-    if constexpr (N1 > 0) store_scaled<N1>(s1, t, lane, z1, inv1);
-    const int64_t own_slot = (static_cast<int64_t>(p.rank) * p.T + t) * 4;
+    store_scaled<N0>(s0, ws.col0, t, lane, z0, inv0);
+    if constexpr (N1 > 0) store_scaled<N1>(s1, ws.col1, t, lane, z1, inv1);
+    const int64_t own_slot = (static_cast<int64_t>(ws.rank) * p.T + t) * 4;
     if constexpr (MODE == kFused) {
       st4f_lane0(own0, make_rsrc_at(s0.partials, own_slot, 4u), lane);
       if constexpr (N1 > 0) st4f_lane0(own1, make_rsrc_at(s1.partials, own_slot, 4u), lane);
     }
-    st4f_lane0(inv0, make_rsrc_at(s0.inv_rms, t * 4, 4u), lane);
-    if constexpr (N1 > 0) st4f_lane0(inv1, make_rsrc_at(s1.inv_rms, t * 4, 4u), lane);
+    st4f_lane0(inv0, make_rsrc_at(s0.inv_rms, (ws.inv_row + t) * 4, 4u), lane);
+    if constexpr (N1 > 0) st4f_lane0(inv1, make_rsrc_at(s1.inv_rms, (ws.inv_row + t) * 4, 4u), lane);
   }
 }
 
@@ -390,9 +475,21 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
   constexpr int M1 = N1 > 0 ? N1 : 1;
   const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
   const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (blockDim.x / kWave);
-  const int own_rank = (MODE == kFused) ? p.rank : -1;
-
-  const int64_t w = wave_index();
+  bool given_up = false;
+  int64_t w = wave_index();
+  int64_t nw = nwaves;
+  WaveSlice ws{p.rank, 0, 0, 0};
+  if constexpr (MODE == kFusedWait) {
+    if (p.group > 1) {  // the grid is a multiple of the group size
+      ws.rank = static_cast<int>(w % p.group);
+      w /= p.group;
+      nw /= p.group;
+      ws.col0 = static_cast<int64_t>(ws.rank) * p.seg[0].d;
+      ws.col1 = static_cast<int64_t>(ws.rank) * p.seg[1].d;
+      ws.inv_row = static_cast<int64_t>(ws.rank) * p.T;
+    }
+  }
+  const int own_rank = (MODE == kFused || MODE == kFusedWait) ? ws.rank : -1;
   int64_t t, step, end;
   if (p.tok_chunk > 0) {
     t = w * p.tok_chunk;
@@ -400,41 +497,41 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
     end = (t + p.tok_chunk < p.T) ? t + p.tok_chunk : p.T;
   } else {
     t = w;
-    step = nwaves;
+    step = nw;
     end = p.T;
   }
   if (t >= end) return;
 
   f32x4 g0[N0][2];
   f32x4 g1[M1][2];
-  if constexpr (MODE != kPartial) {
-    load_gamma<N0>(p.seg[0], lane, g0);
-    if constexpr (N1 > 0) load_gamma<N1>(p.seg[1], lane, g1);
+  if constexpr (MODE != kPartial && MODE != kPublish) {
+    load_gamma<N0>(p.seg[0], ws.col0, lane, g0);
+    if constexpr (N1 > 0) load_gamma<N1>(p.seg[1], ws.col1, lane, g1);
   }
 
   TokenRegs<N0, M1> ra;
-  fetch_token<N0, N1, MODE>(p, t, lane, own_rank, ra);
+  fetch_token<N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
   if constexpr (PF) {
     TokenRegs<N0, M1> rb;
     const int64_t last = end - 1;
     while (true) {
       int64_t tn = t + step;
-      fetch_token<N0, N1, MODE>(p, tn < last ? tn : last, lane, own_rank, rb);
-      process_token<N0, N1, MODE>(p, t, lane, own_rank, g0, g1, ra);
+      fetch_token<N0, N1, MODE>(p, ws, tn < last ? tn : last, lane, own_rank, rb);
+      process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
       if (tn > last) break;
       t = tn;
       tn = t + step;
-      fetch_token<N0, N1, MODE>(p, tn < last ? tn : last, lane, own_rank, ra);
-      process_token<N0, N1, MODE>(p, t, lane, own_rank, g0, g1, rb);
+      fetch_token<N0, N1, MODE>(p, ws, tn < last ? tn : last, lane, own_rank, ra);
+      process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, rb, given_up);
       if (tn > last) break;
       t = tn;
     }
   } else {
     while (true) {
-      process_token<N0, N1, MODE>(p, t, lane, own_rank, g0, g1, ra);
+      process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
       t += step;
       if (t >= end) break;
-      fetch_token<N0, N1, MODE>(p, t, lane, own_rank, ra);
+      fetch_token<N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
     }
   }
 }
@@ -556,17 +653,21 @@ const RowsFn kFusedTable[2][4][5] = {
      QKN_ROW_SET(kFused, 8, true)}};
 const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(kApply, false), QKN_ONE_SET(kApply, true)};
 const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(kPartial, false), QKN_ONE_SET(kPartial, true)};
+const RowsFn kFusedWaitTable[4][5] = {
+    QKN_ROW_SET(kFusedWait, 1, false), QKN_ROW_SET(kFusedWait, 2, false),
+    QKN_ROW_SET(kFusedWait, 4, false), QKN_ROW_SET(kFusedWait, 8, false)};
+const RowsFn kPublishTable[4] = QKN_ONE_SET(kPublish, false);
 const GenericFn kGenericTable[3] = {qkn_generic<kFused>, qkn_generic<kApply>,
                                     qkn_generic<kPartial>};
 
-const char* const kModeName[3] = {"fused", "apply", "partial"};
+const char* const kModeName[5] = {"fused", "apply", "partial", "fused_wait", "publish"};
 
 // Static names "rows<N0,N1>/mode" (or "rows_pf<...>" when pipelined).
 const char* rows_name(int mode, int pf, int i0, int i1) {
-  static char names[3][2][4][5][40];
+  static char names[5][2][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
-    for (int m = 0; m < 3; ++m)
+    for (int m = 0; m < 5; ++m)
       for (int f = 0; f < 2; ++f)
         for (int a = 0; a < 4; ++a)
           for (int b = 0; b < 5; ++b)
@@ -692,7 +793,7 @@ struct Planned {
 int check_seg_shape(const qkn_seg& s, int mode) {
   if (!s.x) return QKN_EINVAL;
   if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local) return QKN_EINVAL;
-  if (mode != kPartial) {
+  if (mode != kPartial && mode != kPublish) {
     if (!s.w || !s.y) return QKN_EINVAL;
     if (s.d_full < s.d_local || s.ldy < s.d_local) return QKN_EINVAL;
   }
@@ -702,15 +803,17 @@ int check_seg_shape(const qkn_seg& s, int mode) {
 // Overlap rules: outputs (y, own statistic slots, inv_rms) may not overlap any
 // input or another output, except y == x with equal strides (in place) and a
 // segment's own slots inside its own partials array.
-int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, int mode) {
+int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, int mode,
+                   const Span* extra = nullptr, int nextra = 0) {
   struct Item {
     Span s;
     bool out;
     int seg;
-    int kind;  // 0 x, 1 w, 2 partials (read), 3 y, 4 own slots, 5 inv
+    int kind;  // 0 x, 1 w, 2 partials (read), 3 y, 4 own slots, 5 inv, 6 extra output
   };
-  Item items[12];
+  Item items[16];
   int n = 0;
+  for (int i = 0; i < nextra; ++i) items[n++] = Item{extra[i], true, 100 + i, 6};
   for (int i = 0; i < nseg; ++i) {
     const qkn_seg& s = segs[i];
     items[n++] = Item{bf16_span(s.x, T, s.ldx, s.d_local), false, i, 0};
@@ -718,6 +821,7 @@ int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, i
       items[n++] = Item{f32_span(s.partials, T), true, i, 4};
       continue;
     }
+    if (mode == kPublish) continue;
     items[n++] = Item{f32_span(s.w, s.d_local), false, i, 1};
     if (s.partials) {
       if (mode == kApply || tp > 1) items[n++] = Item{f32_span(s.partials, tp * T), false, i, 2};
@@ -745,7 +849,7 @@ int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, i
 
 bool seg_vec_ok(const qkn_seg& s, int mode) {
   if (!aligned16(s.x) || (s.ldx % kChunk) || (s.d_local % kChunk)) return false;
-  if (mode != kPartial) {
+  if (mode != kPartial && mode != kPublish) {
     if (!aligned16(s.y) || !aligned16(s.w) || (s.ldy % kChunk)) return false;
   }
   return true;
@@ -759,16 +863,26 @@ DevSeg to_dev(const qkn_seg& s, int mode) {
   d.y = s.y;
   d.inv_rms = s.inv_rms;
   d.ldx = s.ldx;
-  d.ldy = (mode == kPartial) ? 0 : s.ldy;
+  d.ldy = (mode == kPartial || mode == kPublish) ? 0 : s.ldy;
   d.d = static_cast<int32_t>(s.d_local);
   d.nchunks = static_cast<int32_t>((s.d_local + kChunk - 1) / kChunk);
-  d.d_full = static_cast<float>(mode == kPartial ? s.d_local : s.d_full);
+  d.d_full = static_cast<float>((mode == kPartial || mode == kPublish) ? s.d_local : s.d_full);
   d.vec = seg_vec_ok(s, mode) ? 1 : 0;
   return d;
 }
 
+// Arguments of the waiting and publishing modes.
+struct WaitArgs {
+  uint64_t* slots[2];
+  int32_t* status;
+  int64_t spin_limit;
+  uint32_t epoch;
+  int co_resident;  // kernels sharing the GPU that wait on each other
+  int group;        // > 1: every rank of the group in this launch
+};
+
 int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps, int mode,
-           void* stream) {
+           void* stream, const WaitArgs* wa = nullptr) {
   KParams kp;
   memset(&kp, 0, sizeof(kp));
   kp.T = T;
@@ -776,6 +890,16 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   kp.tp = tp;
   kp.rank = rank;
   kp.eps = eps;
+  const bool waits = (mode == kFusedWait || mode == kPublish);
+  if (waits) {
+    kp.slots[0] = wa->slots[0];
+    kp.slots[1] = wa->slots[1];
+    kp.status = wa->status;
+    kp.spin_limit = wa->spin_limit;
+    kp.epoch = wa->epoch;
+    kp.group = wa->group;
+  }
+  const int group = (waits && wa->group > 1) ? wa->group : 1;
   bool fast = (g_opt_force_generic == 0) && tp <= kMaxFastTp &&
               static_cast<__int128>(tp) * T * 4 < (static_cast<__int128>(1) << 31);
   int idx[2] = {0, 0};
@@ -788,11 +912,16 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
     if (kp.seg[i].nchunks > max_chunks) max_chunks = kp.seg[i].nchunks;
   }
 
+  if (waits && !fast) return QKN_ENOTSUP;  // the flagged-slot modes exist on the register path only
   const void* fn;
   const char* name;
   int lds = 0;
   int32_t stage_elems = 0;
-  if (fast) {
+  if (waits) {
+    if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
+    else fn = reinterpret_cast<const void*>(kPublishTable[idx[0]]);
+    name = rows_name(mode, 0, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+  } else if (fast) {
     const int pf = g_opt_prefetch ? 1 : 0;
     if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[pf][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
     else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[pf][idx[0]]);
@@ -815,7 +944,7 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   int rc = query_device(&dev, &cus);
   if (rc != QKN_OK) return rc;
   int wpb = 1;
-  if (fast && g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
+  if (fast && !waits && g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
   const int block = wpb * kWave;
   int bpc = 0;
   rc = blocks_per_cu(dev, fn, block, lds, &bpc);
@@ -831,9 +960,23 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
     if (want < waves_per_cu) waves_per_cu = want;
   }
   if (g_opt_waves_per_cu > 0) waves_per_cu = g_opt_waves_per_cu;
+  if (mode == kFusedWait) {
+    // every wavefront of every co-resident waiting kernel must be resident at
+    // once, or a spinning one could hold the place of the one it waits for
+    const int64_t fit = static_cast<int64_t>(bpc) * wpb / wa->co_resident;
+    if (waves_per_cu > fit) waves_per_cu = fit;
+  }
   if (waves_per_cu < 1) waves_per_cu = 1;
   int64_t waves = waves_per_cu * cus;
-  if (waves > T) waves = T;
+  if (group > 1) {
+    // all ranks of the group share the resident wavefronts equally
+    int64_t per_rank = waves / group;
+    if (per_rank > T) per_rank = T;
+    if (per_rank < 1) return QKN_ENOTSUP;  // the group does not fit on the GPU at once
+    waves = per_rank * group;
+  } else if (waves > T) {
+    waves = T;
+  }
   int64_t grid = (waves + wpb - 1) / wpb;
   if (grid > 0x7fffffff) grid = 0x7fffffff;
   if (fast && g_opt_token_blocks) kp.tok_chunk = (T + grid * wpb - 1) / (grid * wpb);
@@ -931,6 +1074,113 @@ int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, 
   return launch(segs, nseg, tp, rank, T, eps, kFused, stream);
 }
 
+int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                         uint64_t* slots_out, uint32_t epoch, void* stream) {
+  if (T < 0 || d_local < 1 || d_local > kMaxWidth || ldx < d_local) return QKN_EINVAL;
+  if (T == 0) return QKN_OK;
+  if (!x || !slots_out || epoch == 0 || (reinterpret_cast<uintptr_t>(slots_out) & 7u))
+    return QKN_EINVAL;
+  qkn_seg s;
+  memset(&s, 0, sizeof(s));
+  s.x = x;
+  s.ldx = ldx;
+  s.d_local = d_local;
+  s.d_full = d_local;
+  const Span out{reinterpret_cast<uintptr_t>(slots_out), 1, T, T, 8};
+  int rc = check_overlaps(&s, 1, 1, 0, T, kPublish, &out, 1);
+  if (rc != QKN_OK) return rc;
+  WaitArgs wa;
+  memset(&wa, 0, sizeof(wa));
+  wa.slots[0] = slots_out;
+  wa.epoch = epoch;
+  wa.spin_limit = 1;
+  wa.co_resident = 1;
+  wa.group = 1;
+  return launch(&s, 1, 1, 0, T, 0.0f, kPublish, stream, &wa);
+}
+
+int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
+                         const qkn_wait* wait, void* stream) {
+  if (!segs || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
+  int rc = validate_common(T, eps, tp, rank);
+  if (rc != QKN_OK) return rc;
+  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  for (int i = 0; i < nseg; ++i) {
+    const qkn_seg& s = segs[i];
+    if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
+        s.ldy < s.d_local)
+      return QKN_EINVAL;
+  }
+  if (T == 0) return QKN_OK;
+  if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
+  Span extra[3];
+  int nextra = 0;
+  for (int i = 0; i < nseg; ++i) {
+    rc = check_seg_shape(segs[i], kFusedWait);
+    if (rc != QKN_OK) return rc;
+    if (segs[i].partials) return QKN_EINVAL;  // statistics travel in wait->slots
+    uint64_t* sl = wait->slots[i];
+    if (!sl || (reinterpret_cast<uintptr_t>(sl) & 7u)) return QKN_EINVAL;
+    extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
+  }
+  extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
+  rc = check_overlaps(segs, nseg, tp, rank, T, kFusedWait, extra, nextra);
+  if (rc != QKN_OK) return rc;
+  WaitArgs wa;
+  wa.slots[0] = wait->slots[0];
+  wa.slots[1] = nseg == 2 ? wait->slots[1] : nullptr;
+  wa.status = wait->status;
+  wa.spin_limit = wait->spin_limit;
+  wa.epoch = wait->epoch;
+  wa.co_resident = wait->co_resident;
+  wa.group = 1;
+  return launch(segs, nseg, tp, rank, T, eps, kFusedWait, stream, &wa);
+}
+
+int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float eps,
+                         const qkn_wait* wait, void* stream) {
+  if (!segs || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
+  int rc = validate_common(T, eps, tp, 0);
+  if (rc != QKN_OK) return rc;
+  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  qkn_seg view[2];  // the full tensors, for shape and overlap checks
+  for (int i = 0; i < nseg; ++i) {
+    const qkn_seg& s = segs[i];
+    if (s.d_local < 1 || s.d_local > kMaxWidth || s.d_full != s.d_local * tp ||
+        s.ldx < s.d_full || s.ldy < s.d_full)
+      return QKN_EINVAL;
+    view[i] = s;
+    view[i].d_local = s.d_full;
+    view[i].inv_rms = nullptr;
+  }
+  if (T == 0) return QKN_OK;
+  if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
+  Span extra[5];
+  int nextra = 0;
+  for (int i = 0; i < nseg; ++i) {
+    rc = check_seg_shape(view[i], kFusedWait);
+    if (rc != QKN_OK) return rc;
+    if (segs[i].partials) return QKN_EINVAL;
+    uint64_t* sl = wait->slots[i];
+    if (!sl || (reinterpret_cast<uintptr_t>(sl) & 7u)) return QKN_EINVAL;
+    extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
+    if (segs[i].inv_rms)
+      extra[nextra++] = Span{reinterpret_cast<uintptr_t>(segs[i].inv_rms), 1, tp * T, tp * T, 4};
+  }
+  extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
+  rc = check_overlaps(view, nseg, tp, 0, T, kFusedWait, extra, nextra);
+  if (rc != QKN_OK) return rc;
+  WaitArgs wa;
+  wa.slots[0] = wait->slots[0];
+  wa.slots[1] = nseg == 2 ? wait->slots[1] : nullptr;
+  wa.status = wait->status;
+  wa.spin_limit = wait->spin_limit;
+  wa.epoch = wait->epoch;
+  wa.co_resident = wait->co_resident;
+  wa.group = tp;
+  return launch(segs, nseg, tp, 0, T, eps, kFusedWait, stream, &wa);
+}
+
 int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream) {
   if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
   for (int i = 0; i < nseg; ++i)
@@ -944,6 +1194,7 @@ const char* qkn_strerror(int status) {
     case QKN_EINVAL: return "invalid argument";
     case QKN_EOVERLAP: return "output overlaps an input or another output";
     case QKN_EHIP: return "HIP runtime error";
+    case QKN_ENOTSUP: return "shape or alignment not supported by this entry point";
     default: return "unknown status";
   }
 }

@@ -251,3 +251,125 @@ def test_options(lib):
     assert lib.qkn_set_option(b"waves_per_block", 5) == L.QKN_EINVAL
     assert lib.qkn_set_option(b"no_such_key", 1) == L.QKN_EINVAL
     assert lib.qkn_set_option(None, 1) == L.QKN_EINVAL
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """ctypes mirrors of the C structs have the header's sizes and offsets."""
+    import shutil
+    import subprocess
+    if not shutil.which("gcc"):
+        pytest.skip("no C compiler")
+    src = tmp_path / "layout.c"
+    src.write_text('''#include <stdio.h>
+#include <stddef.h>
+#include "qkn.h"
+#define F(T, m) printf(#T "." #m " %zu\\n", offsetof(T, m))
+int main(void) {
+  printf("qkn_seg %zu\\n", sizeof(qkn_seg)); F(qkn_seg, x); F(qkn_seg, ldx); F(qkn_seg, w);
+  F(qkn_seg, partials); F(qkn_seg, y); F(qkn_seg, ldy); F(qkn_seg, inv_rms);
+  F(qkn_seg, d_local); F(qkn_seg, d_full);
+  printf("qkn_wait %zu\\n", sizeof(qkn_wait)); F(qkn_wait, slots); F(qkn_wait, epoch);
+  F(qkn_wait, spin_limit); F(qkn_wait, co_resident); F(qkn_wait, status);
+  printf("qkn_launch_info %zu\\n", sizeof(qkn_launch_info)); F(qkn_launch_info, kernel);
+  F(qkn_launch_info, grid); F(qkn_launch_info, block); F(qkn_launch_info, waves);
+  F(qkn_launch_info, lds_bytes);
+  return 0;
+}
+''')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)],
+                   check=True)
+    c = dict(line.rsplit(" ", 1) for line in
+             subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+             if line)
+    for name, cls in (("qkn_seg", L.QknSeg), ("qkn_wait", L.QknWait),
+                      ("qkn_launch_info", L.QknLaunchInfo)):
+        assert int(c[name]) == ctypes.sizeof(cls), name
+        for field, _ in cls._fields_:
+            assert int(c[f"{name}.{field}"]) == getattr(cls, field).offset, (name, field)
+
+
+def _wait_block(**kw):
+    base = dict(slots=(BASE + 512 * MB, BASE + 600 * MB), epoch=1, spin_limit=1000,
+                co_resident=1, status=BASE + 700 * MB)
+    base.update(kw)
+    return L.QknWait((ctypes.c_void_p * 2)(*base["slots"]), base["epoch"], base["spin_limit"],
+                     base["co_resident"], base["status"])
+
+
+def _fused_wait(lib, segs, tp, rank, T, wait):
+    arr = (L.QknSeg * len(segs))(*segs)
+    return lib.qkn_fused_shard_wait(arr, len(segs), tp, rank, T, ctypes.c_float(1e-6),
+                                    ctypes.byref(wait) if wait is not None else None, None)
+
+
+def _q_nopart():
+    q = _q()
+    q.partials = None
+    return q
+
+
+def _k_nopart():
+    k = _k()
+    k.partials = None
+    return k
+
+
+def test_wait_entry_validation(dry):
+    ok = _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block())
+    assert ok == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<2,1>/fused_wait"
+    for kw in (dict(epoch=0), dict(spin_limit=0), dict(co_resident=0), dict(status=None),
+               dict(status=BASE + 700 * MB + 2), dict(slots=(None, BASE + 600 * MB)),
+               dict(slots=(BASE + 512 * MB + 4, BASE + 600 * MB))):
+        assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block(**kw)) == \
+            L.QKN_EINVAL, kw
+    assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, None) == L.QKN_EINVAL
+    # statistics must travel in the slots, not in partials
+    assert _fused_wait(dry, [_q(), _k_nopart()], 4, 1, 64, _wait_block()) == L.QKN_EINVAL
+    # slot arrays overlapping each other or an output
+    assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64,
+                       _wait_block(slots=(BASE + 512 * MB, BASE + 512 * MB + 64))) == L.QKN_EOVERLAP
+    assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64,
+                       _wait_block(slots=(BASE + 128 * MB, BASE + 600 * MB))) == L.QKN_EOVERLAP
+    # outside the register path
+    odd = _seg(BASE, 100, BASE + 64 * MB, None, BASE + 128 * MB, 100, 100, 400)
+    assert _fused_wait(dry, [odd], 4, 1, 64, _wait_block()) == L.QKN_ENOTSUP
+    # zero tokens: nothing to do
+    assert _fused_wait(dry, [_q_nopart()], 4, 1, 0, _wait_block(status=None)) == 0
+
+
+def test_publish_entry_validation(dry):
+    assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/publish"
+    assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB, 0, None) == L.QKN_EINVAL
+    assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB + 4, 7, None) == L.QKN_EINVAL
+    assert dry.qkn_publish_partials(None, 1024, 64, 1024, BASE + 512 * MB, 7, None) == L.QKN_EINVAL
+    assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 64, 7, None) == L.QKN_EOVERLAP
+    assert dry.qkn_publish_partials(BASE, 100, 64, 100, BASE + 512 * MB, 7, None) == L.QKN_ENOTSUP
+    assert dry.qkn_publish_partials(BASE, 1024, 0, 1024, None, 0, None) == 0
+
+
+def test_group_entry_validation(dry):
+    T = 64
+
+    def full(d_local, tp, ld=None):
+        ld = ld or d_local * tp
+        return _seg(BASE, ld, BASE + 64 * MB, None, BASE + 128 * MB, ld, d_local, d_local * tp)
+
+    def call(segs, tp, wait):
+        arr = (L.QknSeg * len(segs))(*segs)
+        return dry.qkn_fused_group_wait(arr, len(segs), tp, T, ctypes.c_float(1e-6),
+                                        ctypes.byref(wait), None)
+    assert call([full(1024, 4)], 4, _wait_block()) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows<2,0>/fused_wait"
+    bad = full(1024, 4)
+    bad.d_full = 4000
+    assert call([bad], 4, _wait_block()) == L.QKN_EINVAL           # d_full != tp * d_local
+    assert call([full(1024, 4, ld=2048)], 4, _wait_block()) == L.QKN_EINVAL  # ld < d_full
+    withp = full(1024, 4)
+    withp.partials = BASE + 900 * MB
+    assert call([withp], 4, _wait_block()) == L.QKN_EINVAL
+    # the slot array over the full x (T x 4096 bf16 = 512 KiB from BASE)
+    assert call([full(1024, 4)], 4, _wait_block(slots=(BASE + 4096, None))) == L.QKN_EOVERLAP
+    assert call([full(100, 4)], 4, _wait_block()) == L.QKN_ENOTSUP

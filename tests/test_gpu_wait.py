@@ -1,0 +1,166 @@
+"""GPU: the fused kernel waiting for concurrently published statistics.
+
+A rank's fused kernel publishes its own statistics as flagged slots and spins
+(bounded) until the other ranks' slots of each token carry the round's epoch.
+Other ranks are emulated on one GPU either by publishing kernels on another
+stream (issued first: kernels on separate streams are not guaranteed to run
+concurrently on one GPU) or by running every rank of the group in one launch,
+where all wavefronts are resident together. Results must be bit-identical to
+qkn_fused_shard given the same statistics. Every wait is bounded by a spin
+limit, so a failure shows up as status = 1 and NaN outputs, never as a hang;
+the time-out case is forced from the host by never publishing.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from paper_2608_09160_amd import _lib as L
+
+from gpu_util import DEV, bits_of, inputs, run_fused_rank, to_dev_bf16, to_dev_f32
+
+pytestmark = pytest.mark.gpu
+
+SPIN = 1 << 21  # polls per slot: ~1 s at most, far above any legitimate wait here
+
+
+def _rank_inputs(wl, data, rank):
+    segs, peers = [], []
+    for key, gkey, d_full in (("xq", "gq", wl.q_full), ("xk", "gk", wl.k_full)):
+        cols = workloads.shard_cols(d_full, wl.tp, rank)
+        segs.append(L.Seg(x=to_dev_bf16(data[key][:, cols]), w=to_dev_f32(data[gkey][cols]),
+                          d_full=d_full, inv_rms=torch.empty(wl.T, dtype=torch.float32, device=DEV)))
+        peers.append([to_dev_bf16(data[key][:, workloads.shard_cols(d_full, wl.tp, k)])
+                      for k in range(wl.tp)])
+    return segs, peers
+
+
+def _slot_arrays(wl):
+    return [torch.zeros((wl.tp, wl.T), dtype=torch.int64, device=DEV) for _ in range(2)]
+
+
+def _check_against_fused(wl, data, rank, segs):
+    ref = run_fused_rank(wl, data, rank)
+    for s, t in zip(segs, "qk"):
+        assert np.array_equal(bits_of(s.y), ref[t]["y"]), (rank, t)
+        assert np.array_equal(s.inv_rms.cpu().numpy(), ref[t]["inv"]), (rank, t)
+
+
+def test_producers_and_consumer_on_separate_streams():
+    """Peers publish from another stream; the consumer uses whatever it finds,
+    waiting where a slot is not there yet. (Kernels on separate streams are not
+    guaranteed to run at the same time on one GPU, so the producers are issued
+    first: the consumer may or may not have to wait, and must be right either way.)"""
+    wl = workloads.DECODE_TP4
+    data = inputs(wl)
+    rank = 1
+    segs, peers = _rank_inputs(wl, data, rank)
+    slots = _slot_arrays(wl)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s_cons, s_prod = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    print("[wait] producers, then consumer, on two streams", flush=True)
+    with torch.cuda.stream(s_prod):
+        for k in range(wl.tp):
+            if k != rank:
+                for i in range(2):
+                    L.qkn_publish_partials(peers[i][k], slots[i][k], 1)
+    with torch.cuda.stream(s_cons):
+        L.qkn_fused_shard_wait(segs, wl.tp, rank, wl.eps, slots, epoch=1, spin_limit=SPIN,
+                               co_resident=2, status=status)
+    assert L.qkn_last_launch()["kernel"].endswith("/fused_wait")
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    _check_against_fused(wl, data, rank, segs)
+    # the own slots were published with the epoch and the Phase A value
+    own = slots[0][rank].cpu().numpy().view(np.uint64)
+    assert np.all((own >> np.uint64(32)) == 1)
+    alone = L.qkn_partial_sumsq(peers[0][rank]).cpu().numpy()
+    assert np.array_equal((own & np.uint64(0xFFFFFFFF)).astype(np.uint32).view(np.float32), alone)
+
+
+GROUPS = [workloads.DECODE_TP4, workloads.DECODE_TP8, workloads.PREFILL_TP2.with_tokens(2048),
+          workloads.Workload("tp3_T300_q1536_k384", 300, 1536, 384, 3, "normal", 7),
+          workloads.PREFILL_TP2, workloads.LONG_PREFILL_TP4]
+
+
+@pytest.mark.parametrize("wl", GROUPS, ids=lambda w: w.name)
+def test_whole_group_in_one_launch(wl):
+    """Every rank of the group in one launch: each wavefront publishes its rank's
+    statistic and waits for the others'; all of them are resident at once."""
+    data = inputs(wl)
+    slots = _slot_arrays(wl)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    segs = [L.Seg(x=to_dev_bf16(data[key]), w=to_dev_f32(data[gkey]), d_full=d_full,
+                  inv_rms=torch.empty((wl.tp, wl.T), dtype=torch.float32, device=DEV))
+            for key, gkey, d_full in (("xq", "gq", wl.q_full), ("xk", "gk", wl.k_full))]
+    torch.cuda.synchronize()
+    print(f"[wait] group of {wl.tp} in one launch: {wl.name}", flush=True)
+    for epoch in (11, 12):  # a second round reuses the slots with a new epoch
+        L.qkn_fused_group_wait(segs, wl.tp, wl.eps, slots, epoch=epoch, spin_limit=SPIN,
+                               status=status)
+        info = L.qkn_last_launch()
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        assert info["kernel"].endswith("/fused_wait") and info["waves"] % wl.tp == 0
+    ranks = range(wl.tp) if wl.T <= 2048 else (0, wl.tp - 1)
+    for r in ranks:
+        ref = run_fused_rank(wl, data, r)
+        for s, t, d_full in zip(segs, "qk", (wl.q_full, wl.k_full)):
+            cols = workloads.shard_cols(d_full, wl.tp, r)
+            assert np.array_equal(bits_of(s.y[:, cols]), ref[t]["y"]), (r, t)
+            assert np.array_equal(s.inv_rms[r].cpu().numpy(), ref[t]["inv"]), (r, t)
+
+
+def test_timeout_when_nobody_publishes():
+    wl = workloads.DECODE_TP4
+    data = inputs(wl)
+    segs, _ = _rank_inputs(wl, data, 2)
+    slots = _slot_arrays(wl)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    torch.cuda.synchronize()
+    print("[wait] forced time-out (no producer, 64 polls)", flush=True)
+    L.qkn_fused_shard_wait(segs, wl.tp, 2, wl.eps, slots, epoch=9, spin_limit=64,
+                           co_resident=1, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 1
+    for s in segs:
+        assert torch.isnan(s.y.float()).all()
+    # this rank still published its own statistics
+    own = slots[1][2].cpu().numpy().view(np.uint64)
+    assert np.all((own >> np.uint64(32)) == 9)
+
+
+def test_epochs_reuse_slots_without_reset():
+    wl = workloads.DECODE_TP8
+    data = inputs(wl)
+    rank = 6
+    segs, peers = _rank_inputs(wl, data, rank)
+    slots = _slot_arrays(wl)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for epoch in (5, 6):
+        for s in segs:
+            if s.y is not None:
+                s.y.zero_()
+        torch.cuda.synchronize()
+        print(f"[wait] epoch {epoch}", flush=True)
+        with torch.cuda.stream(torch.cuda.Stream()):
+            for k in range(wl.tp):
+                if k != rank:
+                    for i in range(2):
+                        L.qkn_publish_partials(peers[i][k], slots[i][k], epoch)
+        torch.cuda.synchronize()
+        L.qkn_fused_shard_wait(segs, wl.tp, rank, wl.eps, slots, epoch=epoch, spin_limit=SPIN,
+                               co_resident=1, status=status)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        _check_against_fused(wl, data, rank, segs)
+    # a round whose statistics never arrive does not use the previous round's
+    print("[wait] stale epoch", flush=True)
+    L.qkn_fused_shard_wait(segs, wl.tp, rank, wl.eps, slots, epoch=7, spin_limit=64,
+                           co_resident=1, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 1
+    assert torch.isnan(segs[0].y.float()).all()
