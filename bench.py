@@ -118,6 +118,41 @@ class Case:
             self.L.qkn_apply(s.x, s.w, s.partials, s.d_full, self.wl.eps, y=s.y)
 
 
+class GroupCase:
+    """Every rank of a tp group in one launch (qkn_fused_group_wait) over the full
+    Q/K tensors, rotating buffer sets; each launch is one round (new epoch)."""
+
+    def __init__(self, wl, min_footprint, torch, L, data):
+        self.wl, self.torch, self.L = wl, torch, L
+        dev = "cuda:0"
+
+        def bf16(a):
+            a = np.ascontiguousarray(a, dtype=np.uint16)
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        xs = [bf16(data["xq"]), bf16(data["xk"])]
+        ws = [torch.from_numpy(data["gq"]).to(dev), torch.from_numpy(data["gk"]).to(dev)]
+        set_bytes = sum(2 * x.numel() * 2 for x in xs)
+        self.nsets = max(2, -(-min_footprint // set_bytes))
+        self.sets = []
+        for i in range(self.nsets):
+            segs = [L.Seg(x=x.clone() if i else x, w=w, d_full=x.shape[1], y=torch.empty_like(x))
+                    for x, w in zip(xs, ws)]
+            slots = [torch.zeros((wl.tp, wl.T), dtype=torch.int64, device=dev) for _ in range(2)]
+            self.sets.append((segs, slots))
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.epoch = 0
+        T, tp = wl.T, wl.tp
+        # x read + y written, gamma, per rank: own slot written, tp - 1 slots read (8 B each)
+        self.bytes = sum(2 * T * d * 2 + 4 * d + 8 * T * tp * tp for d in (wl.q_full, wl.k_full))
+        torch.cuda.synchronize()
+
+    def launch(self, i):
+        segs, slots = self.sets[i % self.nsets]
+        self.epoch += 1
+        self.L.qkn_fused_group_wait(segs, self.wl.tp, self.wl.eps, slots, epoch=self.epoch,
+                                    spin_limit=1 << 22, status=self.status)
+
+
 def time_region(torch, fn, steps, warmup):
     """Wall time (ms) of `steps` back-to-back calls between two events on the stream."""
     stream = torch.cuda.current_stream()
@@ -381,6 +416,16 @@ def main():
                                      "kernel_us": round(fk * 1e3, 3),
                                      "gbs": round(fcase.bytes / (fk * 1e-3) / 1e9, 1)}
         del fcase
+        # the Phase B wait: every rank of the tp group in one launch, each wavefront
+        # publishing its statistic and waiting for the others' (same data as tp = 1)
+        gcase = GroupCase(wl, min_fp, torch, L, data)
+        gk = time_region(torch, gcase.launch, args.steps, args.warmup) / args.steps
+        gstatus = int(gcase.status.item())
+        extras["group_wait_all_ranks"] = {"kernel": L.qkn_last_launch()["kernel"],
+                                          "bytes": gcase.bytes, "kernel_us": round(gk * 1e3, 3),
+                                          "gbs": round(gcase.bytes / (gk * 1e-3) / 1e9, 1),
+                                          "status": gstatus}
+        del gcase
         # decode shapes: one launch replayed from a HIP graph (inputs cache-warm,
         # as right after the projection that produced them)
         lat = {}

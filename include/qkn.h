@@ -233,6 +233,8 @@ int qkn_last_launch(qkn_launch_info* info);
  *                    persistent);
  *   "prefetch"       1 = pipelined kernels that request the next token
  *                    before writing the current one, 0 = not (default);
+ *   "balance"        1 = shrink the grid so every wavefront takes the same
+ *                    number of tokens, 0 = use the full grid (default);
  *   "token_blocks"   1 = each wavefront takes a contiguous range of tokens,
  *                    0 = tokens strided by the wavefront count (default);
  *   "waves_per_block" 1..4, 0 = automatic;

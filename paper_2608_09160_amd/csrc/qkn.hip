@@ -253,10 +253,11 @@ __device__ __forceinline__ void load_gamma(const DevSeg& s, int64_t col, int lan
   }
 }
 
+// `live` false: an empty descriptor -- every lane reads zeros, nothing is fetched.
 template <int N>
 __device__ __forceinline__ void load_row(const DevSeg& s, int64_t col, int64_t t, int lane,
-                                         u32x4 (&x)[N]) {
-  const Rsrc r = make_rsrc(s.x + t * s.ldx + col, static_cast<uint32_t>(s.nchunks) * 16u);
+                                         u32x4 (&x)[N], bool live = true) {
+  const Rsrc r = make_rsrc(s.x + t * s.ldx + col, live ? static_cast<uint32_t>(s.nchunks) * 16u : 0u);
 #pragma unroll
   for (int i = 0; i < N; ++i) x[i] = ld16_nt(r, (i * kWave + lane) * 16);
 }
@@ -265,9 +266,9 @@ __device__ __forceinline__ void load_row(const DevSeg& s, int64_t col, int64_t t
 // from slot t of rank 0); the rank's own slot `skip` and lanes >= tp are out of
 // range and read 0. The register path requires tp * T * 4 < 2^31.
 __device__ __forceinline__ float load_slots_buf(const float* partials, int64_t T, int64_t t,
-                                                int lane, int tp, int skip) {
+                                                int lane, int tp, int skip, bool live = true) {
   const uint32_t nrec = static_cast<uint32_t>((tp - 1) * T * 4 + 4);
-  const Rsrc r = make_rsrc_at(partials, t * 4, nrec);
+  const Rsrc r = make_rsrc_at(partials, t * 4, live ? nrec : 0u);
   const int off = (lane < tp && lane != skip) ? static_cast<int>(lane * T * 4)
                                               : static_cast<int>(nrec);
   return ld4f(r, off);
@@ -324,29 +325,46 @@ __device__ __forceinline__ void publish_slot(uint64_t* slot, float v, uint32_t e
 // Lanes 0..tp-1 other than `rank` poll rank k's slot of token t until it
 // carries `epoch`, at most `limit` times (with a short sleep between polls).
 // A lane that gives up, or any lane once `given_up` is set, returns NaN.
+// `first` is the slot's word as read when the token's rows were requested (see
+// poll_slots); only a lane whose slot was not ready yet polls again.
 __device__ __forceinline__ float wait_slot(const uint64_t* slots, int64_t T, int64_t t, int lane,
                                            int tp, int rank, uint32_t epoch, int64_t limit,
-                                           bool given_up, bool& gave_up_now) {
+                                           bool given_up, uint64_t first, bool& gave_up_now) {
   float v = 0.0f;
   if (lane < tp && lane != rank) {
     v = __builtin_nanf("");
     if (!given_up) {
       const uint64_t* slot = slots + static_cast<int64_t>(lane) * T + t;
-      for (int64_t n = 0;;) {
-        const uint64_t word = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      uint64_t word = first;
+      for (int64_t n = 1;;) {
         if (static_cast<uint32_t>(word >> 32) == epoch) {
           v = __builtin_bit_cast(float, static_cast<uint32_t>(word));
           break;
         }
-        if (++n >= limit) {
+        if (n++ >= limit) {
           gave_up_now = true;
           break;
         }
         __builtin_amdgcn_s_sleep(1);
+        word = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
   }
   return v;
+}
+
+// First poll of the other ranks' slots of token t, issued with the token's rows:
+// lanes 0..tp-1 (not `rank`) read slot lane*T + t with one 64-bit agent-coherent
+// load each (the same single-copy-atomic access as the relaxed atomic load);
+// other lanes are out of range and read 0, which no epoch matches.
+constexpr int kCoherentCpol = 16;  // sc1: bypass the CU-local cache
+__device__ __forceinline__ uint64_t poll_slots(const uint64_t* slots, int64_t T, int64_t t,
+                                               int lane, int tp, int rank, bool live) {
+  const uint32_t nrec = static_cast<uint32_t>(((tp - 1) * T + 1) * 8);
+  const Rsrc r = make_rsrc_at(slots, t * 8, live ? nrec : 0u);
+  const int off = (lane < tp && lane != rank) ? static_cast<int>(lane * T * 8)
+                                              : static_cast<int>(nrec);
+  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherentCpol));
 }
 
 // The rank a wavefront computes and where that rank's slice sits: the launch's
@@ -365,20 +383,30 @@ struct TokenRegs {
   u32x4 x1[M1];
   float slots0;
   float slots1;
+  uint64_t word0;  // wait mode: first poll of the other ranks' slots
+  uint64_t word1;
 };
 
+// `live` false (a pipelined request past the last token): nothing is fetched.
 template <int N0, int N1, int MODE>
 __device__ __forceinline__ void fetch_token(const KParams& p, const WaveSlice& ws, int64_t t,
                                             int lane, int own_rank,
-                                            TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r) {
-  load_row<N0>(p.seg[0], ws.col0, t, lane, r.x0);
-  if constexpr (N1 > 0) load_row<N1>(p.seg[1], ws.col1, t, lane, r.x1);
+                                            TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
+                                            bool live = true) {
+  load_row<N0>(p.seg[0], ws.col0, t, lane, r.x0, live);
+  if constexpr (N1 > 0) load_row<N1>(p.seg[1], ws.col1, t, lane, r.x1, live);
   r.slots0 = 0.0f;
   r.slots1 = 0.0f;
   if constexpr (MODE == kFused || MODE == kApply) {
     // with tp == 1 (fused) every lane is out of range: nothing is read
-    r.slots0 = load_slots_buf(p.seg[0].partials, p.T, t, lane, p.tp, own_rank);
-    if constexpr (N1 > 0) r.slots1 = load_slots_buf(p.seg[1].partials, p.T, t, lane, p.tp, own_rank);
+    r.slots0 = load_slots_buf(p.seg[0].partials, p.T, t, lane, p.tp, own_rank, live);
+    if constexpr (N1 > 0)
+      r.slots1 = load_slots_buf(p.seg[1].partials, p.T, t, lane, p.tp, own_rank, live);
+  }
+  if constexpr (MODE == kFusedWait) {
+    r.word0 = poll_slots(p.slots[0], p.T, t, lane, p.tp, own_rank, live);
+    r.word1 = 0;
+    if constexpr (N1 > 0) r.word1 = poll_slots(p.slots[1], p.T, t, lane, p.tp, own_rank, live);
   }
 }
 
@@ -432,10 +460,10 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
     if constexpr (MODE == kFusedWait) {
       bool gave_up = false;
       slots0 = wait_slot(p.slots[0], p.T, t, lane, p.tp, ws.rank, p.epoch, p.spin_limit, given_up,
-                         gave_up);
+                         r.word0, gave_up);
       if constexpr (N1 > 0)
         slots1 = wait_slot(p.slots[1], p.T, t, lane, p.tp, ws.rank, p.epoch, p.spin_limit,
-                           given_up || gave_up, gave_up);
+                           given_up || gave_up, r.word1, gave_up);
       if (__ballot(gave_up) != 0) {
         if (!given_up && lane == 0)
           __hip_atomic_store(p.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -468,10 +496,11 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
 // token's rows and slots are requested before the current token is reduced
 // and written, so each wavefront keeps two tokens in flight. Two register sets
 // alternate roles (the loop is unrolled by two) so that no copy forces a wait
-// on the requests in flight; the next-token index is clamped to the last token
-// so every request is unconditional.
-template <int N0, int N1, int MODE, bool PF>
+// on the requests in flight; past the last token the request goes through an
+// empty descriptor, so it is unconditional and fetches nothing.
+template <int N0, int N1, int MODE, int SCHED>
 __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
+  constexpr bool PF = (SCHED == 1);
   constexpr int M1 = N1 > 0 ? N1 : 1;
   const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
   const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (blockDim.x / kWave);
@@ -516,12 +545,12 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
     const int64_t last = end - 1;
     while (true) {
       int64_t tn = t + step;
-      fetch_token<N0, N1, MODE>(p, ws, tn < last ? tn : last, lane, own_rank, rb);
+      fetch_token<N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, rb, tn <= last);
       process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
       if (tn > last) break;
       t = tn;
       tn = t + step;
-      fetch_token<N0, N1, MODE>(p, ws, tn < last ? tn : last, lane, own_rank, ra);
+      fetch_token<N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, ra, tn <= last);
       process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, rb, given_up);
       if (tn > last) break;
       t = tn;
@@ -532,6 +561,102 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
       t += step;
       if (t >= end) break;
       fetch_token<N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ wide rows
+//
+// Slices wider than the register path holds with gamma (d_local in (4096,
+// 16384], aligned as for the register path). One wavefront per token with
+// both tensors' rows in VGPRs (N0 / N1 chunks per lane, all requested at
+// once; the launcher puts the wide tensor in slot 0). gamma of both tensors is
+// staged in LDS once per workgroup and read from there in Phase C, which forms
+// (x * gamma) * factor -- the same operations, order and reduction tree as
+// every other path.
+
+// Phase C of one wide row from gamma in LDS: y = bf16((x * gamma) * inv).
+template <int N>
+__device__ __forceinline__ void store_scaled_lds(const DevSeg& s, int64_t t, int lane,
+                                                 const u32x4 (&x)[N], const f32x4* g, float inv) {
+  const Rsrc ry = make_rsrc(s.y + t * s.ldy, static_cast<uint32_t>(s.nchunks) * 16u);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int c = i * kWave + lane;
+    const int cc = c < s.nchunks ? c : 0;  // masked lanes: any in-range gamma, store dropped
+    const f32x4 ga = g[2 * cc], gb = g[2 * cc + 1];
+    u32x4 o;
+    o[0] = pack_bf16x2((bf16_lo(x[i][0]) * ga[0]) * inv, (bf16_hi(x[i][0]) * ga[1]) * inv);
+    o[1] = pack_bf16x2((bf16_lo(x[i][1]) * ga[2]) * inv, (bf16_hi(x[i][1]) * ga[3]) * inv);
+    o[2] = pack_bf16x2((bf16_lo(x[i][2]) * gb[0]) * inv, (bf16_hi(x[i][2]) * gb[1]) * inv);
+    o[3] = pack_bf16x2((bf16_lo(x[i][3]) * gb[2]) * inv, (bf16_hi(x[i][3]) * gb[3]) * inv);
+    st16_nt(o, ry, c * 16);
+    // keep the scheduler from hoisting every chunk's gamma reads (register pressure)
+    if ((i & 1) == 1) __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int N0, int N1, int MODE>
+__global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
+  extern __shared__ __align__(16) float gamma_lds[];  // [d0 + d1] (fused / apply)
+  constexpr int M1 = N1 > 0 ? N1 : 1;
+  const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (blockDim.x / kWave);
+  const int own_rank = (MODE == kFused) ? p.rank : -1;
+  const DevSeg& s0 = p.seg[0];
+  const DevSeg& s1 = p.seg[1];
+
+  if constexpr (MODE != kPartial) {
+    // stage gamma: 16 bytes per thread per step, both tensors back to back
+    const int n0 = s0.d / 4;
+    const int n1 = (N1 > 0) ? s1.d / 4 : 0;
+    f32x4* dst = reinterpret_cast<f32x4*>(gamma_lds);
+    for (int i = static_cast<int>(threadIdx.x); i < n0 + n1; i += static_cast<int>(blockDim.x)) {
+      dst[i] = (i < n0) ? reinterpret_cast<const f32x4*>(s0.w)[i]
+                        : reinterpret_cast<const f32x4*>(s1.w)[i - n0];
+    }
+    __syncthreads();
+  }
+  const f32x4* g0 = reinterpret_cast<const f32x4*>(gamma_lds);
+  const f32x4* g1 = g0 + s0.d / 4;
+
+  for (int64_t t = wave_index(); t < p.T; t += nwaves) {
+    u32x4 x0[N0];
+    u32x4 x1[M1];
+    load_row<N0>(s0, 0, t, lane, x0);
+    if constexpr (N1 > 0) load_row<N1>(s1, 0, t, lane, x1);
+    float sl0 = 0.0f, sl1 = 0.0f;
+    if constexpr (MODE != kPartial) {
+      sl0 = load_slots_buf(s0.partials, p.T, t, lane, p.tp, own_rank);
+      if constexpr (N1 > 0) sl1 = load_slots_buf(s1.partials, p.T, t, lane, p.tp, own_rank);
+    }
+    float own0 = 0.0f, own1 = 0.0f;
+    if constexpr (MODE != kApply) {
+      own0 = wave_sum(row_lane_sumsq<N0>(x0));
+      if constexpr (N1 > 0) own1 = wave_sum(row_lane_sumsq<N1>(x1));
+    }
+    if constexpr (MODE == kPartial) {
+      st4f_lane0(own0, make_rsrc_at(s0.partials, t * 4, 4u), lane);
+    } else {
+      const float inv0 = rms_inverse(combine_slots(sl0, own0, p.tp, own_rank), s0.d_full, p.eps);
+      float inv1 = 0.0f;
+      if constexpr (N1 > 0)
+        inv1 = rms_inverse(combine_slots(sl1, own1, p.tp, own_rank), s1.d_full, p.eps);
+      // Re-derive the fp32 values from the packed rows instead of keeping the
+      // unpacked ones alive from Phase A (an empty asm hides x's value; no code).
+#pragma unroll
+      for (int i = 0; i < N0; ++i) asm volatile("" : "+v"(x0[i]));
+#pragma unroll
+      for (int i = 0; i < M1; ++i) asm volatile("" : "+v"(x1[i]));
+      store_scaled_lds<N0>(s0, t, lane, x0, g0, inv0);
+      if constexpr (N1 > 0) store_scaled_lds<N1>(s1, t, lane, x1, g1, inv1);
+      const int64_t own_slot = (static_cast<int64_t>(p.rank) * p.T + t) * 4;
+      if constexpr (MODE == kFused) {
+        st4f_lane0(own0, make_rsrc_at(s0.partials, own_slot, 4u), lane);
+        if constexpr (N1 > 0) st4f_lane0(own1, make_rsrc_at(s1.partials, own_slot, 4u), lane);
+      }
+      st4f_lane0(inv0, make_rsrc_at(s0.inv_rms, t * 4, 4u), lane);
+      if constexpr (N1 > 0) st4f_lane0(inv1, make_rsrc_at(s1.inv_rms, t * 4, 4u), lane);
     }
   }
 }
@@ -639,44 +764,65 @@ typedef void (*GenericFn)(KParams, int32_t);
 constexpr int kNIdx[9] = {-1, 0, 1, 2, 2, 3, 3, 3, 3};  // chunks/lane -> table index
 constexpr int kNVal[4] = {1, 2, 4, 8};
 
-#define QKN_ROW_SET(M, A, PF)                                                          \
-  {qkn_rows<A, 0, M, PF>, qkn_rows<A, 1, M, PF>, qkn_rows<A, 2, M, PF>,                 \
-   qkn_rows<A, 4, M, PF>, qkn_rows<A, 8, M, PF>}
-#define QKN_ONE_SET(M, PF) \
-  {qkn_rows<1, 0, M, PF>, qkn_rows<2, 0, M, PF>, qkn_rows<4, 0, M, PF>, qkn_rows<8, 0, M, PF>}
+#define QKN_ROW_SET(M, A, S)                                                           \
+  {qkn_rows<A, 0, M, S>, qkn_rows<A, 1, M, S>, qkn_rows<A, 2, M, S>, qkn_rows<A, 4, M, S>, \
+   qkn_rows<A, 8, M, S>}
+#define QKN_ONE_SET(M, S) \
+  {qkn_rows<1, 0, M, S>, qkn_rows<2, 0, M, S>, qkn_rows<4, 0, M, S>, qkn_rows<8, 0, M, S>}
+#define QKN_FULL_SET(M, S) \
+  {QKN_ROW_SET(M, 1, S), QKN_ROW_SET(M, 2, S), QKN_ROW_SET(M, 4, S), QKN_ROW_SET(M, 8, S)}
 
-// [prefetch][N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
-const RowsFn kFusedTable[2][4][5] = {
-    {QKN_ROW_SET(kFused, 1, false), QKN_ROW_SET(kFused, 2, false), QKN_ROW_SET(kFused, 4, false),
-     QKN_ROW_SET(kFused, 8, false)},
-    {QKN_ROW_SET(kFused, 1, true), QKN_ROW_SET(kFused, 2, true), QKN_ROW_SET(kFused, 4, true),
-     QKN_ROW_SET(kFused, 8, true)}};
-const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(kApply, false), QKN_ONE_SET(kApply, true)};
-const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(kPartial, false), QKN_ONE_SET(kPartial, true)};
-const RowsFn kFusedWaitTable[4][5] = {
-    QKN_ROW_SET(kFusedWait, 1, false), QKN_ROW_SET(kFusedWait, 2, false),
-    QKN_ROW_SET(kFusedWait, 4, false), QKN_ROW_SET(kFusedWait, 8, false)};
-const RowsFn kPublishTable[4] = QKN_ONE_SET(kPublish, false);
+// Schedules: 0 one token per step, 1 pipelined (next token requested early).
+// [schedule][N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
+const RowsFn kFusedTable[2][4][5] = {QKN_FULL_SET(kFused, 0), QKN_FULL_SET(kFused, 1)};
+const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(kApply, 0), QKN_ONE_SET(kApply, 1)};
+const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(kPartial, 0), QKN_ONE_SET(kPartial, 1)};
+const RowsFn kFusedWaitTable[2][4][5] = {QKN_FULL_SET(kFusedWait, 0),
+                                         QKN_FULL_SET(kFusedWait, 1)};
+const RowsFn kPublishTable[4] = QKN_ONE_SET(kPublish, 0);
 const GenericFn kGenericTable[3] = {qkn_generic<kFused>, qkn_generic<kApply>,
                                     qkn_generic<kPartial>};
+constexpr int kMaxWideChunks = 32;  // chunks per lane on the wide path (d_local <= 16384)
+constexpr int kMaxWideLdsBytes = 64 * 1024;
+#define QKN_WIDE_SET(A, M) \
+  {qkn_wide<A, 0, M>, qkn_wide<A, 1, M>, qkn_wide<A, 2, M>, qkn_wide<A, 4, M>, qkn_wide<A, 8, M>}
+// [wide N0: 16, 32][mode][N1 index: 0 = single segment, then 1, 2, 4, 8]
+const RowsFn kWideTable[2][3][5] = {
+    {QKN_WIDE_SET(16, kFused), QKN_WIDE_SET(16, kApply), QKN_WIDE_SET(16, kPartial)},
+    {QKN_WIDE_SET(32, kFused), QKN_WIDE_SET(32, kApply), QKN_WIDE_SET(32, kPartial)}};
 
 const char* const kModeName[5] = {"fused", "apply", "partial", "fused_wait", "publish"};
 
-// Static names "rows<N0,N1>/mode" (or "rows_pf<...>" when pipelined).
-const char* rows_name(int mode, int pf, int i0, int i1) {
+// Static names "rows<N0,N1>/mode" ("rows_pf<...>" when pipelined).
+const char* rows_name(int mode, int sched, int i0, int i1) {
   static char names[5][2][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
+    const char* const prefix[2] = {"rows", "rows_pf"};
     for (int m = 0; m < 5; ++m)
       for (int f = 0; f < 2; ++f)
         for (int a = 0; a < 4; ++a)
           for (int b = 0; b < 5; ++b)
-            snprintf(names[m][f][a][b], sizeof(names[m][f][a][b]), "%s<%d,%d>/%s",
-                     f ? "rows_pf" : "rows", kNVal[a], b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
+            snprintf(names[m][f][a][b], sizeof(names[m][f][a][b]), "%s<%d,%d>/%s", prefix[f],
+                     kNVal[a], b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
   });
-  return names[mode][pf][i0][i1];
+  return names[mode][sched][i0][i1];
 }
 const char* const kGenericName[3] = {"generic/fused", "generic/apply", "generic/partial"};
+
+// Static names "wide<N0,N1>/mode".
+const char* wide_name(int mode, int i0, int i1) {
+  static char names[3][2][5][40];
+  static std::once_flag once;
+  std::call_once(once, [] {
+    for (int m = 0; m < 3; ++m)
+      for (int a = 0; a < 2; ++a)
+        for (int b = 0; b < 5; ++b)
+          snprintf(names[m][a][b], sizeof(names[m][a][b]), "wide<%d,%d>/%s", a ? 32 : 16,
+                   b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
+  });
+  return names[mode][i0][i1];
+}
 
 // Options.
 int64_t g_opt_waves_per_cu = 0;
@@ -685,6 +831,7 @@ int64_t g_opt_force_generic = 0;
 int64_t g_opt_validate_only = 0;
 int64_t g_opt_prefetch = 0;
 int64_t g_opt_token_blocks = 0;
+int64_t g_opt_balance = 0;
 
 thread_local qkn_launch_info t_last = {nullptr, 0, 0, 0, 0};
 
@@ -900,16 +1047,40 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
     kp.group = wa->group;
   }
   const int group = (waits && wa->group > 1) ? wa->group : 1;
-  bool fast = (g_opt_force_generic == 0) && tp <= kMaxFastTp &&
-              static_cast<__int128>(tp) * T * 4 < (static_cast<__int128>(1) << 31);
+  const bool buffer_ok = (g_opt_force_generic == 0) && tp <= kMaxFastTp &&
+                         static_cast<__int128>(tp) * T * 4 < (static_cast<__int128>(1) << 31);
+  bool fast = buffer_ok;
+  bool wide = buffer_ok && !waits;
   int idx[2] = {0, 0};
-  int max_chunks = 0;
+  int max_chunks = 0, max_per_lane = 0;
+  int64_t gamma_floats = 0;
   for (int i = 0; i < nseg; ++i) {
     kp.seg[i] = to_dev(segs[i], mode);
     const int per_lane = (kp.seg[i].nchunks + kWave - 1) / kWave;
     if (!kp.seg[i].vec || per_lane > kMaxRegChunks) fast = false;
     else idx[i] = kNIdx[per_lane];
+    if (!kp.seg[i].vec || per_lane > kMaxWideChunks) wide = false;
     if (kp.seg[i].nchunks > max_chunks) max_chunks = kp.seg[i].nchunks;
+    if (per_lane > max_per_lane) max_per_lane = per_lane;
+    gamma_floats += kp.seg[i].d;
+  }
+  if (fast) wide = false;
+  if (mode != kPartial && gamma_floats * 4 > kMaxWideLdsBytes) wide = false;
+  int wide_i0 = 0, wide_i1 = 0;
+  if (wide) {
+    // the wider tensor goes first (slot 0 holds up to 32 chunks per lane, slot 1 up to 8)
+    if (nseg == 2 && kp.seg[1].nchunks > kp.seg[0].nchunks) {
+      const DevSeg tmp = kp.seg[0];
+      kp.seg[0] = kp.seg[1];
+      kp.seg[1] = tmp;
+    }
+    const int pl0 = (kp.seg[0].nchunks + kWave - 1) / kWave;
+    wide_i0 = pl0 <= 16 ? 0 : 1;
+    if (nseg == 2) {
+      const int pl1 = (kp.seg[1].nchunks + kWave - 1) / kWave;
+      if (pl1 > kMaxRegChunks) wide = false;  // both tensors wide: general path
+      else wide_i1 = kNIdx[pl1] + 1;
+    }
   }
 
   if (waits && !fast) return QKN_ENOTSUP;  // the flagged-slot modes exist on the register path only
@@ -917,16 +1088,21 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   const char* name;
   int lds = 0;
   int32_t stage_elems = 0;
-  if (waits) {
-    if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
+  if (wide) {
+    fn = reinterpret_cast<const void*>(kWideTable[wide_i0][mode][wide_i1]);
+    name = wide_name(mode, wide_i0, wide_i1);
+    lds = (mode == kPartial) ? 0 : static_cast<int>(gamma_floats * 4);
+  } else if (waits) {
+    const int sched = (mode == kFusedWait && g_opt_prefetch) ? 1 : 0;
+    if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[sched][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
     else fn = reinterpret_cast<const void*>(kPublishTable[idx[0]]);
-    name = rows_name(mode, 0, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+    name = rows_name(mode, sched, idx[0], nseg == 2 ? idx[1] + 1 : 0);
   } else if (fast) {
-    const int pf = g_opt_prefetch ? 1 : 0;
-    if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[pf][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
-    else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[pf][idx[0]]);
-    else fn = reinterpret_cast<const void*>(kPartialTable[pf][idx[0]]);
-    name = rows_name(mode, pf, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+    const int sched = g_opt_prefetch ? 1 : 0;
+    if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[sched][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
+    else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[sched][idx[0]]);
+    else fn = reinterpret_cast<const void*>(kPartialTable[sched][idx[0]]);
+    name = rows_name(mode, sched, idx[0], nseg == 2 ? idx[1] + 1 : 0);
   } else {
     fn = reinterpret_cast<const void*>(kGenericTable[mode]);
     name = kGenericName[mode];
@@ -945,6 +1121,7 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   if (rc != QKN_OK) return rc;
   int wpb = 1;
   if (fast && !waits && g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
+  if (wide) wpb = 4;  // four wavefronts share the gamma staged in LDS
   const int block = wpb * kWave;
   int bpc = 0;
   rc = blocks_per_cu(dev, fn, block, lds, &bpc);
@@ -952,7 +1129,7 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   // Persistent grid: enough wavefronts per CU to keep about kInFlightBytes of
   // rows requested per CU, at least kMinWavesPerCu, at most what fits.
   int64_t waves_per_cu = static_cast<int64_t>(bpc) * wpb;
-  if (fast) {
+  if ((fast || wide) && mode != kFusedWait) {  // a waiting launch keeps every resident slot
     int64_t token_bytes = 0;
     for (int i = 0; i < nseg; ++i) token_bytes += 2 * static_cast<int64_t>(kp.seg[i].d);
     int64_t want = (kInFlightBytes + token_bytes - 1) / token_bytes;
@@ -976,15 +1153,20 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
     waves = per_rank * group;
   } else if (waves > T) {
     waves = T;
+  } else if (fast && g_opt_balance) {
+    // equal shares: k tokens per wavefront for every wavefront (but the last),
+    // so that none runs an extra token while the others are done
+    const int64_t k = (T + waves - 1) / waves;
+    waves = (T + k - 1) / k;
   }
   int64_t grid = (waves + wpb - 1) / wpb;
   if (grid > 0x7fffffff) grid = 0x7fffffff;
   if (fast && g_opt_token_blocks) kp.tok_chunk = (T + grid * wpb - 1) / (grid * wpb);
 
   hipError_t err;
-  if (fast) {
+  if (fast || wide) {
     void* args[] = {&kp};
-    err = hipLaunchKernel(fn, dim3(static_cast<unsigned>(grid)), dim3(block), args, 0,
+    err = hipLaunchKernel(fn, dim3(static_cast<unsigned>(grid)), dim3(block), args, lds,
                           static_cast<hipStream_t>(stream));
   } else {
     void* args[] = {&kp, &stage_elems};
@@ -1219,6 +1401,9 @@ int qkn_set_option(const char* key, int64_t value) {
   } else if (strcmp(key, "prefetch") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_prefetch = value;
+  } else if (strcmp(key, "balance") == 0) {
+    if (value != 0 && value != 1) return QKN_EINVAL;
+    g_opt_balance = value;
   } else if (strcmp(key, "token_blocks") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_token_blocks = value;

@@ -91,13 +91,36 @@ def test_valid_calls_pass_validation(dry):
 
 @pytest.mark.parametrize("d,expect", [(8, "<1,0>"), (512, "<1,0>"), (520, "<2,0>"),
                                       (2048, "<4,0>"), (1536, "<4,0>"),
-                                      (4096, "<8,0>"), (4104, "generic"),
-                                      (100, "generic"), (1, "generic")])
+                                      (4096, "<8,0>"), (4104, "wide<16,0>"), (8192, "wide<16,0>"),
+                                      (8200, "wide<32,0>"), (16384, "wide<32,0>"),
+                                      (16392, "generic"), (100, "generic"), (1, "generic")])
 def test_path_choice_by_width(dry, d, expect):
     seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
     assert _fused(dry, [seg], 2, 0, 16) == 0
     name = L.qkn_last_launch()["kernel"]
-    assert name.startswith("generic") if expect == "generic" else (name.startswith("rows") and expect in name)
+    if expect in ("generic",) or expect.startswith("wide"):
+        assert name.startswith(expect), name
+    else:
+        assert name.startswith("rows") and expect in name, name
+
+
+def test_wide_path_needs_gamma_to_fit_lds(dry):
+    q = _seg(BASE, 16384, BASE + 640 * MB, BASE + 641 * MB, BASE + 256 * MB, 16384, 16384, 16384)
+    k = _seg(BASE + 512 * MB, 1024, BASE + 642 * MB, BASE + 643 * MB, BASE + 700 * MB, 1024, 1024, 1024)
+    assert _fused(dry, [q, k], 1, 0, 16) == 0   # 17408 gamma floats > 64 KiB of LDS
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
+    q = _seg(BASE, 8192, BASE + 640 * MB, BASE + 641 * MB, BASE + 256 * MB, 8192, 8192, 8192)
+    assert _fused(dry, [q, k], 1, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "wide<16,2>/fused"
+    assert L.qkn_last_launch()["lds_bytes"] == (8192 + 1024) * 4
+    # the wide tensor may come second: the launcher puts it in slot 0
+    assert _fused(dry, [k, q], 1, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "wide<16,2>/fused"
+    # both tensors wide: the general path
+    k2 = _seg(BASE + 512 * MB, 5120, BASE + 642 * MB, BASE + 643 * MB, BASE + 700 * MB, 5120, 5120, 5120)
+    q2 = _seg(BASE, 5120, BASE + 640 * MB, BASE + 641 * MB, BASE + 256 * MB, 5120, 5120, 5120)
+    assert _fused(dry, [q2, k2], 1, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic/fused"
 
 
 def test_prefetch_option_selects_variant(dry):

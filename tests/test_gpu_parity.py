@@ -84,6 +84,29 @@ def test_full_vector_matches_oracle(wl):
                         compare.PARTIAL_RTOL, "q full sum")
 
 
+@pytest.mark.parametrize("wl", [workloads.LONG_PREFILL_TP4.with_tp(1).with_tokens(777),
+                                workloads.DECODE_TP8.with_tp(1)], ids=lambda w: w.name)
+def test_wide_full_vector_matches_oracle(wl):
+    """tp = 1 with Q wider than the register path (8192 and 5120 columns)."""
+    data = inputs(wl)
+    print(f"[parity] wide full {wl.name}", flush=True)
+    out = run_fused_rank(wl, data, 0)
+    assert out["launch"]["kernel"].startswith("wide<16,2>"), out["launch"]
+    ref = Q.qknorm_layerwise(data["xq"], data["xk"], data["gq"], data["gk"], 1, 0, wl.eps)
+    for t in "qk":
+        compare.check_close(Q.decode_bf16(out[t]["y"]), ref[t]["y"], compare.OUTPUT_RTOL, t)
+        compare.check_close(out[t]["partials"][0], ref[t]["partials"][0], compare.PARTIAL_RTOL, t)
+    # the general kernel gives the same bits
+    L.qkn_set_option("force_generic", 1)
+    try:
+        gen = run_fused_rank(wl, data, 0)
+    finally:
+        L.qkn_set_option("force_generic", 0)
+    assert gen["launch"]["kernel"] == "generic/fused"
+    for t in "qk":
+        assert np.array_equal(gen[t]["y"], out[t]["y"]) and np.array_equal(gen[t]["inv"], out[t]["inv"])
+
+
 def test_tp_invariance():
     """One oracle, every TP degree: shards at tp 1, 2, 4, 8 all agree with it."""
     base = workloads.PREFILL_TP2.with_tokens(300)
@@ -221,7 +244,9 @@ def _oracle_single(x_full_bits, gamma_full, tp, rank, eps):
 
 @pytest.mark.parametrize("T,d_local,tp", [(1, 1, 1), (3, 7, 2), (33, 100, 3), (70, 4104, 2),
                                           (9, 20000, 1), (5, 40000, 2), (130, 8, 4),
-                                          (67, 4096, 2), (64, 520, 4), (5, 24, 65), (4, 16, 130)])
+                                          (67, 4096, 2), (64, 520, 4), (5, 24, 65), (4, 16, 130),
+                                          (37, 5120, 1), (300, 8192, 2), (21, 16384, 1),
+                                          (13, 8200, 3)])
 def test_shapes_fast_and_general(T, d_local, tp):
     d_full = d_local * tp
     x_full = workloads.random_rows(T * 7 + d_local, T, d_full, "student_t")
