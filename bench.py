@@ -55,12 +55,13 @@ def parse():
     return p.parse_args()
 
 
-def algorithmic_bytes(T, widths, tp, write_partials=True):
-    """x read once + y written once (bf16) + gamma (fp32) once + own statistic
-    written + the other ranks' statistics read (fp32), per launch."""
+def algorithmic_bytes(T, widths, tp, write_partials=True, esz=2):
+    """x read once + y written once (esz bytes per element: bf16 2, fp8 1) +
+    gamma (fp32) once + own statistic written + the other ranks' statistics
+    read (fp32), per launch."""
     b = 0
     for d in widths:
-        b += 2 * T * d * 2 + 4 * d
+        b += 2 * T * d * esz + 4 * d
         b += 4 * T * (tp - 1)
         if write_partials:
             b += 4 * T
@@ -75,8 +76,14 @@ class Case:
         data = data if data is not None else workloads.generate(wl)
         dev = "cuda:0"
         tp, T = wl.tp, wl.T
+        self.fp8 = wl.dtype == "fp8"
+        self.esz = 1 if self.fp8 else 2
+        self.partial_fn = L.qkn_partial_sumsq_fp8 if self.fp8 else L.qkn_partial_sumsq
+        self.apply_fn = L.qkn_apply_fp8 if self.fp8 else L.qkn_apply
 
         def bf16(a):
+            if self.fp8:  # FP8 codes as uint8 device tensors (the binding takes either dtype)
+                return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).to(dev)
             a = np.ascontiguousarray(a, dtype=np.uint16)
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
 
@@ -90,9 +97,9 @@ class Case:
                 P = torch.zeros((tp, T), dtype=torch.float32, device=dev)
                 for k in range(tp):  # simulated peers (and the own slot, overwritten)
                     xk = x if k == rank else bf16(data[key][:, workloads.shard_cols(d_full, tp, k)])
-                    L.qkn_partial_sumsq(xk, out=P[k])
+                    self.partial_fn(xk, out=P[k])
             shards.append((x, w, P, d_full))
-        set_bytes = sum(2 * x.numel() * 2 for x, _, _, _ in shards)
+        set_bytes = sum(2 * x.numel() * self.esz for x, _, _, _ in shards)
         self.nsets = max(2, -(-min_footprint // set_bytes))
         self.sets = []
         for i in range(self.nsets):
@@ -106,7 +113,8 @@ class Case:
         self.calls = [L.Prepared(segs, tp, rank, wl.eps, full=full) for segs in self.sets]
         torch.cuda.synchronize()
         self.footprint = self.nsets * set_bytes
-        self.bytes = algorithmic_bytes(T, (wl.q_local, wl.k_local), tp, write_partials=P is not None)
+        self.bytes = algorithmic_bytes(T, (wl.q_local, wl.k_local), tp, write_partials=P is not None,
+                                       esz=self.esz)
 
     def launch(self, i):
         self.calls[i % self.nsets]()
@@ -114,8 +122,8 @@ class Case:
     def launch_two_step(self, i):
         """Phase A, then Phases B+C, per tensor: the unfused scalar-statistic path."""
         for s in self.sets[i % self.nsets]:
-            self.L.qkn_partial_sumsq(s.x, out=s.partials[self.rank])
-            self.L.qkn_apply(s.x, s.w, s.partials, s.d_full, self.wl.eps, y=s.y)
+            self.partial_fn(s.x, out=s.partials[self.rank])
+            self.apply_fn(s.x, s.w, s.partials, s.d_full, self.wl.eps, y=s.y)
 
 
 class GroupCase:
@@ -446,6 +454,22 @@ def main():
                                       "kernel_us": round(lk * 1e3, 3),
                                       "gbs": round(lcase.bytes / (lk * 1e-3) / 1e9, 1)}
         del lcase
+        # FP8-E4M3 activations (Sec. IV-C's second format): the same prefill
+        # shard, and the decode shape replayed from a graph
+        f8 = wl.with_dtype("fp8")
+        p8 = Case(f8, args.rank, min_fp, torch, L, workloads)
+        pk = time_region(torch, p8.launch, args.steps, args.warmup) / args.steps
+        extras["fp8_prefill_shard"] = {"kernel": L.qkn_last_launch()["kernel"], "bytes": p8.bytes,
+                                       "kernel_us": round(pk * 1e3, 3),
+                                       "gbs": round(p8.bytes / (pk * 1e-3) / 1e9, 1),
+                                       "frac_of_peak": round(p8.bytes / (pk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        del p8
+        d8 = Case(workloads.DECODE_TP4.with_dtype("fp8"), 0, 0, torch, L, workloads)
+        us = time_graph(torch, lambda i, c=d8: c.launch(0), 200, 10) * 1e3
+        extras["fp8_decode_T64_tp4_graph"] = {"us_per_launch_graph": round(us, 3),
+                                              "kernel": L.qkn_last_launch()["kernel"],
+                                              "bytes": d8.bytes}
+        del d8
         print("[bench] extras done", file=sys.stderr, flush=True)
 
     cpu = None

@@ -18,7 +18,8 @@
  * would arrive over the interconnect).
  *
  * Conventions for every entry point
- *   - bf16 tensors are passed as uint16_t bit patterns; fp32 as float.
+ *   - bf16 tensors are passed as uint16_t bit patterns, FP8-E4M3 tensors (the
+ *     *_fp8 entry points) as uint8_t bit patterns; fp32 as float.
  *   - Every pointer is DEVICE memory, owned by the caller. The library never
  *     allocates or frees device memory and keeps no pointer after returning.
  *   - A row-major tensor [T, ld] uses columns [0, d_local) of each row;
@@ -30,17 +31,19 @@
  *   - Errors are returned as negative status codes; nothing aborts and no C++
  *     exception crosses the ABI. Faults during kernel execution surface, as
  *     usual for HIP, at the caller's next synchronisation.
- *   - Arithmetic: bf16 inputs are widened exactly, all sums and products are
- *     fp32, the output is rounded once to bf16 (nearest, ties to even).
- *     NaN and infinities propagate by IEEE rules (eps = 0 with an all-zero row
- *     gives NaN).
+ *   - Arithmetic: inputs are widened exactly, all sums and products are fp32
+ *     (Sec. IV-C: fp32 accumulation for bf16 and FP8-E4M3 activations), and
+ *     the output is rounded once to the input's format (nearest, ties to
+ *     even). NaN and infinities propagate by IEEE rules (eps = 0 with an
+ *     all-zero row gives NaN).
  *   - Determinism: a row's partial sum depends only on d_local and the row's
  *     values (one fixed fp32 summation tree), never on the launch shape or the
  *     entry point, so every rank combines bit-identical statistics.
- *   - Fast path: 128-bit accesses when x, y are 16-byte aligned, w is 16-byte
- *     aligned, and ld and d_local are multiples of 8, with d_local <= 4096 and
- *     tp <= 64; otherwise a general path gives the same bits, more slowly.
- *     Alignment is never an error.
+ *   - Fast paths: 128-bit accesses when x, y and w are 16-byte aligned and ld
+ *     and d_local are multiples of 8 (bf16) or 16 (fp8), with tp <= 64: rows
+ *     held in registers up to d_local = 4096, wider rows with gamma in LDS up
+ *     to 16384 columns over both tensors together; otherwise a general path
+ *     gives the same bits, more slowly. Alignment is never an error.
  */
 #ifndef QKN_H
 #define QKN_H
@@ -137,6 +140,42 @@ int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, 
 int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream);
 
 /*
+ * FP8-E4M3 activations (Sec. IV-C evaluates SwiftQK on them): the OCP
+ * e4m3fn format -- 1 sign, 4 exponent (bias 7), 3 mantissa bits; largest
+ * finite value 448; no infinities; NaN is S.1111.111. x and y are uint8_t bit
+ * patterns; gamma, statistics and factors are fp32 as above, and every sum
+ * and product is fp32. Inputs decode exactly. The output is
+ * e4m3fn( (x * w) * factor ), rounded to nearest even; a result whose
+ * magnitude rounds above 448 is NaN (the format has no infinity), as in the
+ * usual non-saturating cast. The partial sums of a slice are bit-identical
+ * across these entry points (one fixed tree, as for bf16), so
+ * qkn_partial_sumsq_fp8 serves as a peer rank's contribution to
+ * qkn_fused_shard_fp8. Arguments, errors and overlap rules are those of the
+ * bf16 entry point of the same name, with sizes and strides in elements
+ * (bytes).
+ */
+typedef struct qkn_seg8 {
+  const uint8_t* x;
+  int64_t ldx;
+  const float* w;
+  float* partials;
+  uint8_t* y;
+  int64_t ldy;
+  float* inv_rms;
+  int64_t d_local;
+  int64_t d_full;
+} qkn_seg8;
+
+int qkn_partial_sumsq_fp8(const uint8_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                          float* partial_out, void* stream);
+int qkn_apply_fp8(const uint8_t* x, int64_t ldx, const float* w, const float* partials,
+                  int tp, int64_t T, int64_t d_local, int64_t d_full, float eps,
+                  uint8_t* y, int64_t ldy, float* inv_rms, void* stream);
+int qkn_fused_shard_fp8(const qkn_seg8* segs, int nseg, int tp, int rank, int64_t T,
+                        float eps, void* stream);
+int qkn_full_fp8(const qkn_seg8* segs, int nseg, int64_t T, float eps, void* stream);
+
+/*
  * Published statistics, for ranks that run concurrently (Sec. III-B; Alg. 1
  * Phase B, where each GPU signals its peers and spins on a local flag).
  * A slot is one 8-byte word: the fp32 statistic's bits in the low half and the
@@ -210,7 +249,8 @@ const char* qkn_strerror(int status);
 /*
  * Launch description of the calling thread's most recent successful launch,
  * for tests and benchmarks. kernel is a static string naming the variant
- * ("rows<4,1>/fused", "generic/apply", ...); grid is in workgroups, block in
+ * ("rows<4,1>/fused", "wide<16,2>/fused", "generic/apply", "rows_fp8<2,1>/fused",
+ * ...; the numbers are 16-byte chunks per lane); grid is in workgroups, block in
  * threads, waves = grid * block / 64, lds_bytes is the dynamic LDS per
  * workgroup.
  */
@@ -232,7 +272,8 @@ int qkn_last_launch(qkn_launch_info* info);
  *                    values oversubscribe, which is correct but not
  *                    persistent);
  *   "prefetch"       1 = pipelined kernels that request the next token
- *                    before writing the current one, 0 = not (default);
+ *                    before writing the current one (bf16 register path),
+ *                    0 = not (default);
  *   "balance"        1 = shrink the grid so every wavefront takes the same
  *                    number of tokens, 0 = use the full grid (default);
  *   "token_blocks"   1 = each wavefront takes a contiguous range of tokens,

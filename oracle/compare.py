@@ -7,6 +7,11 @@ Tolerances:
   * bf16 outputs: relative error <= 8e-3 (about two bf16 ulps) per element;
     where the oracle is exactly 0 the result must be exactly 0; NaN must match
     NaN and infinities must match in sign.
+  * FP8-E4M3 outputs (``check_fp8``): the result must be what rounding to
+    nearest gives for some value within a relative FP8_NOISE of the fp64
+    oracle (the fp32 arithmetic before the final rounding is that close), i.e.
+    |y - ref| <= half an FP8 step at |ref| (1 + noise) + noise |ref|; values
+    that round past 448 must be NaN (the format has no infinity).
 Error metrics reported next to them are the three the paper uses against its
 fp64 gold output (Sec. IV-C): maximum, mean and RMS absolute error.
 """
@@ -18,6 +23,9 @@ import numpy as np
 
 PARTIAL_RTOL = 1e-5
 OUTPUT_RTOL = 8e-3
+FP8_NOISE = 1e-5
+E4M3_MAX = 448.0
+E4M3_OVERFLOW = 464.0  # halfway between 448 and the next step, 480, which has no code
 
 
 def rel_error(test: np.ndarray, ref: np.ndarray) -> np.ndarray:
@@ -72,3 +80,54 @@ def paper_error_metrics(test: np.ndarray, ref: np.ndarray) -> Dict[str, float]:
         return {"max_abs": 0.0, "mean_abs": 0.0, "rms_abs": 0.0}
     return {"max_abs": float(d.max()), "mean_abs": float(d.mean()),
             "rms_abs": float(np.sqrt(np.mean(d * d)))}
+
+
+def e4m3_half_step(mag: np.ndarray) -> np.ndarray:
+    """Half the FP8-E4M3 grid step at magnitude `mag` (>= 0).
+
+    Step 2^(k-3) in the binade [2^k, 2^(k+1)) for k >= -6, and 2^-9 below 2^-6
+    (subnormals, same step as the first normal binade).
+    """
+    mag = np.asarray(mag, dtype=np.float64)
+    k = np.frexp(np.where(mag > 0, mag, 1.0))[1] - 1
+    k = np.where(mag > 0, np.maximum(k, -6), -6)
+    return np.exp2(k - 4.0)
+
+
+def check_fp8(test: np.ndarray, ref: np.ndarray, what: str, noise: float = FP8_NOISE) -> float:
+    """Assert that decoded FP8-E4M3 results are ref rounded to nearest, up to `noise`.
+
+    test: the results decoded to fp64; ref: the fp64 oracle. Returns the largest
+    error in units of half an FP8 step (<= 1 + a little when the check passes).
+    """
+    test = np.asarray(test, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if test.shape != ref.shape:
+        raise AssertionError(f"{what}: shape {test.shape} != {ref.shape}")
+    if np.isinf(test).any():
+        raise AssertionError(f"{what}: FP8 results cannot be infinite")
+    mag = np.abs(ref)
+    with np.errstate(invalid="ignore"):
+        must_nan = np.isnan(ref) | (mag * (1 - noise) > E4M3_OVERFLOW)
+        may_nan = must_nan | (mag * (1 + noise) > E4M3_OVERFLOW)
+    nan_t = np.isnan(test)
+    if (must_nan & ~nan_t).any() or (nan_t & ~may_nan).any():
+        bad = np.argwhere((must_nan & ~nan_t) | (nan_t & ~may_nan))[:5]
+        raise AssertionError(f"{what}: NaN mismatch at {bad.tolist()}")
+    fin = ~nan_t & ~must_nan
+    if not fin.any():
+        return 0.0
+    r, t = ref[fin], test[fin]
+    zero = r == 0
+    if (t[zero] != 0).any():
+        raise AssertionError(f"{what}: nonzero result where the oracle is exactly 0")
+    half = e4m3_half_step(np.abs(r) * (1 + noise))
+    err = np.abs(t - r)
+    bound = half + noise * np.abs(r)
+    if not np.all(err <= bound):
+        i = int(np.argmax(err - bound))
+        idx = np.argwhere(fin)[i]
+        raise AssertionError(
+            f"{what}: FP8 result {t[i]!r} is not the rounding of oracle {r[i]!r} "
+            f"at {idx.tolist()} (error {err[i]:.3e} > {bound[i]:.3e})")
+    return float(np.max(err / half))

@@ -6,9 +6,11 @@ pointers and strides, passes torch's current HIP stream, and maps status codes
 to exceptions. There is no fallback: if the library is missing, loading fails
 loudly (build it with ``python -m paper_2608_09160_amd.build``).
 
-Tensors: bf16 activations are ``torch.bfloat16`` 2-D tensors whose last
-dimension is contiguous (any row stride, so column slices of a wider buffer
-work); gamma, partials and inv_rms are ``torch.float32``.
+Tensors: activations are 2-D tensors whose last dimension is contiguous (any
+row stride, so column slices of a wider buffer work): ``torch.bfloat16`` for
+the bf16 entry points, ``torch.float8_e4m3fn`` (or ``torch.uint8`` holding
+e4m3fn bit patterns) for the ``*_fp8`` ones; gamma, partials and inv_rms are
+``torch.float32``.
 """
 from __future__ import annotations
 
@@ -73,13 +75,18 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                          ctypes.POINTER(QknWait), _vp]
     lib.qkn_fused_group_wait.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, ctypes.c_int,
                                          _c_i64, ctypes.c_float, ctypes.POINTER(QknWait), _vp]
+    lib.qkn_partial_sumsq_fp8.argtypes = lib.qkn_partial_sumsq.argtypes
+    lib.qkn_apply_fp8.argtypes = lib.qkn_apply.argtypes
+    lib.qkn_fused_shard_fp8.argtypes = lib.qkn_fused_shard.argtypes
+    lib.qkn_full_fp8.argtypes = lib.qkn_full.argtypes
     lib.qkn_strerror.argtypes = [ctypes.c_int]
     lib.qkn_strerror.restype = ctypes.c_char_p
     lib.qkn_last_launch.argtypes = [ctypes.POINTER(QknLaunchInfo)]
     lib.qkn_set_option.argtypes = [ctypes.c_char_p, _c_i64]
     for name in ("qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
                  "qkn_last_launch", "qkn_set_option", "qkn_publish_partials",
-                 "qkn_fused_shard_wait", "qkn_fused_group_wait"):
+                 "qkn_fused_shard_wait", "qkn_fused_group_wait", "qkn_partial_sumsq_fp8",
+                 "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -96,10 +103,18 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _rows(t: torch.Tensor, what: str):
-    """(pointer, leading dimension, T, width) of a bf16 [T, width] tensor."""
-    if t.dtype != torch.bfloat16:
-        raise TypeError(f"{what}: expected torch.bfloat16, got {t.dtype}")
+BF16, FP8 = "bf16", "fp8"
+_DTYPES = {BF16: (torch.bfloat16,), FP8: (torch.float8_e4m3fn, torch.uint8)}
+
+
+def _fmt_of(t: torch.Tensor) -> str:
+    return FP8 if t.dtype in _DTYPES[FP8] else BF16
+
+
+def _rows(t: torch.Tensor, what: str, fmt: str = BF16):
+    """(pointer, leading dimension, T, width) of a [T, width] activation tensor."""
+    if t.dtype not in _DTYPES[fmt]:
+        raise TypeError(f"{what}: expected {' or '.join(map(str, _DTYPES[fmt]))}, got {t.dtype}")
     if t.dim() != 2:
         raise ValueError(f"{what}: expected a 2-D [T, d] tensor, got shape {tuple(t.shape)}")
     if t.shape[1] > 1 and t.stride(1) != 1:
@@ -126,60 +141,83 @@ def qkn_strerror(status: int) -> str:
     return load().qkn_strerror(status).decode()
 
 
-def qkn_partial_sumsq(x: torch.Tensor, out: Optional[torch.Tensor] = None,
-                      stream=None) -> torch.Tensor:
-    """Phase A: out[t] = sum_j x[t, j]^2 (fp32) for a bf16 [T, d_local] tensor."""
-    px, ldx, T, d = _rows(x, "x")
+def _partial(fmt, x, out, stream):
+    name = "qkn_partial_sumsq" + ("_fp8" if fmt == FP8 else "")
+    px, ldx, T, d = _rows(x, "x", fmt)
     if out is None:
         out = torch.empty(T, dtype=torch.float32, device=x.device)
     po = _f32(out, "out", T)
-    _check(load().qkn_partial_sumsq(px, ldx, T, d, po, _stream(stream)), "qkn_partial_sumsq")
+    _check(getattr(load(), name)(px, ldx, T, d, po, _stream(stream)), name)
     return out
+
+
+def qkn_partial_sumsq(x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """Phase A: out[t] = sum_j x[t, j]^2 (fp32) for a bf16 [T, d_local] tensor."""
+    return _partial(BF16, x, out, stream)
+
+
+def qkn_partial_sumsq_fp8(x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                          stream=None) -> torch.Tensor:
+    """Phase A for an FP8-E4M3 [T, d_local] tensor."""
+    return _partial(FP8, x, out, stream)
+
+
+def _apply(fmt, x, w, partials, d_full, eps, y, inv_rms, stream):
+    name = "qkn_apply" + ("_fp8" if fmt == FP8 else "")
+    px, ldx, T, d = _rows(x, "x", fmt)
+    if partials.dim() != 2 or partials.shape[1] != T:
+        raise ValueError(f"partials: expected [tp, {T}], got {tuple(partials.shape)}")
+    tp = partials.shape[0]
+    if y is None:
+        y = torch.empty((T, d), dtype=x.dtype, device=x.device)
+    py, ldy, Ty, dy = _rows(y, "y", fmt)
+    if (Ty, dy) != (T, d):
+        raise ValueError("y: shape must match x")
+    _check(getattr(load(), name)(px, ldx, _f32(w, "w", d), _f32(partials, "partials"), tp, T,
+                                 d, d_full, eps, py, ldy, _f32(inv_rms, "inv_rms", T),
+                                 _stream(stream)), name)
+    return y
 
 
 def qkn_apply(x: torch.Tensor, w: torch.Tensor, partials: torch.Tensor, d_full: int,
               eps: float, y: Optional[torch.Tensor] = None,
               inv_rms: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """Phases B+C from all ranks' statistics: partials is fp32 [tp, T] (rank-major)."""
-    px, ldx, T, d = _rows(x, "x")
-    if partials.dim() != 2 or partials.shape[1] != T:
-        raise ValueError(f"partials: expected [tp, {T}], got {tuple(partials.shape)}")
-    tp = partials.shape[0]
-    if y is None:
-        y = torch.empty((T, d), dtype=torch.bfloat16, device=x.device)
-    py, ldy, Ty, dy = _rows(y, "y")
-    if (Ty, dy) != (T, d):
-        raise ValueError("y: shape must match x")
-    _check(load().qkn_apply(px, ldx, _f32(w, "w", d), _f32(partials, "partials"), tp, T, d,
-                            d_full, eps, py, ldy, _f32(inv_rms, "inv_rms", T),
-                            _stream(stream)), "qkn_apply")
-    return y
+    return _apply(BF16, x, w, partials, d_full, eps, y, inv_rms, stream)
+
+
+def qkn_apply_fp8(x: torch.Tensor, w: torch.Tensor, partials: torch.Tensor, d_full: int,
+                  eps: float, y: Optional[torch.Tensor] = None,
+                  inv_rms: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """qkn_apply for FP8-E4M3 activations (x and y)."""
+    return _apply(FP8, x, w, partials, d_full, eps, y, inv_rms, stream)
 
 
 @dataclass
 class Seg:
     """One tensor (Q or K) of one rank for qkn_fused_shard / qkn_full."""
 
-    x: torch.Tensor                  # bf16 [T, d_local] (row stride free)
+    x: torch.Tensor                  # bf16 or fp8 [T, d_local] (row stride free)
     w: torch.Tensor                  # fp32 [d_local]
     d_full: int
-    y: Optional[torch.Tensor] = None  # bf16 [T, d_local]; allocated if None
+    y: Optional[torch.Tensor] = None  # like x, [T, d_local]; allocated if None
     partials: Optional[torch.Tensor] = None  # fp32 [tp, T]
     inv_rms: Optional[torch.Tensor] = None   # fp32 [T]
 
 
-def _segs(segs: Sequence[Seg], tp: int):
-    arr = (QknSeg * len(segs))()
+def _segs(segs: Sequence[Seg], tp: int, fmt: str = BF16):
+    arr = (QknSeg * len(segs))()  # qkn_seg and qkn_seg8 share this layout
     T = None
     for i, s in enumerate(segs):
-        px, ldx, Ts, d = _rows(s.x, f"seg{i}.x")
+        px, ldx, Ts, d = _rows(s.x, f"seg{i}.x", fmt)
         if T is None:
             T = Ts
         elif Ts != T:
             raise ValueError("all segments must have the same number of tokens")
         if s.y is None:
-            s.y = torch.empty((Ts, d), dtype=torch.bfloat16, device=s.x.device)
-        py, ldy, Ty, dy = _rows(s.y, f"seg{i}.y")
+            s.y = torch.empty((Ts, d), dtype=s.x.dtype, device=s.x.device)
+        py, ldy, Ty, dy = _rows(s.y, f"seg{i}.y", fmt)
         if (Ty, dy) != (Ts, d):
             raise ValueError(f"seg{i}.y: shape must match x")
         pp = None
@@ -204,6 +242,21 @@ def qkn_full(segs: Sequence[Seg], eps: float, stream=None):
     """TP = 1 full-vector QK-Norm (d_full == d_local for every segment)."""
     arr, T = _segs(segs, 1)
     _check(load().qkn_full(arr, len(segs), T, eps, _stream(stream)), "qkn_full")
+    return [s.y for s in segs]
+
+
+def qkn_fused_shard_fp8(segs: Sequence[Seg], tp: int, rank: int, eps: float, stream=None):
+    """qkn_fused_shard for FP8-E4M3 activations."""
+    arr, T = _segs(segs, tp, FP8)
+    _check(load().qkn_fused_shard_fp8(arr, len(segs), tp, rank, T, eps, _stream(stream)),
+           "qkn_fused_shard_fp8")
+    return [s.y for s in segs]
+
+
+def qkn_full_fp8(segs: Sequence[Seg], eps: float, stream=None):
+    """qkn_full for FP8-E4M3 activations."""
+    arr, T = _segs(segs, 1, FP8)
+    _check(load().qkn_full_fp8(arr, len(segs), T, eps, _stream(stream)), "qkn_full_fp8")
     return [s.y for s in segs]
 
 
@@ -277,7 +330,8 @@ def qkn_fused_group_wait(segs: Sequence[Seg], tp: int, eps: float,
 
 
 class Prepared:
-    """qkn_fused_shard (or qkn_full) with its argument block marshalled once.
+    """qkn_fused_shard (or qkn_full, or their _fp8 forms, chosen by the
+    activations' dtype) with its argument block marshalled once.
 
     For repeated launches on the same tensors (benchmarks, serving loops):
     calling the object only passes the prepared segment array and the stream.
@@ -286,20 +340,22 @@ class Prepared:
 
     def __init__(self, segs: Sequence[Seg], tp: int, rank: int, eps: float, full: bool = False):
         self.segs = list(segs)
-        self._arr, self._T = _segs(self.segs, tp)
+        fmt = _fmt_of(self.segs[0].x)
+        self._arr, self._T = _segs(self.segs, tp, fmt)
         self._n, self._tp, self._rank = len(self.segs), tp, rank
         self._eps = ctypes.c_float(eps)
         self._full = full
         self._lib = load()
+        self.name = ("qkn_full" if full else "qkn_fused_shard") + ("_fp8" if fmt == FP8 else "")
+        self._fn = getattr(self._lib, self.name)
 
     def __call__(self, stream=None) -> None:
         st = _stream(stream)
         if self._full:
-            rc = self._lib.qkn_full(self._arr, self._n, self._T, self._eps, st)
+            rc = self._fn(self._arr, self._n, self._T, self._eps, st)
         else:
-            rc = self._lib.qkn_fused_shard(self._arr, self._n, self._tp, self._rank, self._T,
-                                           self._eps, st)
-        _check(rc, "qkn_full" if self._full else "qkn_fused_shard")
+            rc = self._fn(self._arr, self._n, self._tp, self._rank, self._T, self._eps, st)
+        _check(rc, self.name)
 
 
 def qkn_last_launch() -> dict:

@@ -7,13 +7,16 @@
 //   Phase A  partial sum of squares of the rank's slice, fp32;
 //   Phase B  ascending-rank sum of all ranks' partials and the factor
 //            1/sqrt(S/H_total + eps); independently of it, x * gamma;
-//   Phase C  the scaled slice, rounded once to bf16 and written.
+//   Phase C  the scaled slice, rounded once to the activation format and written.
+//
+// Activations are bf16 or FP8-E4M3 (OCP e4m3fn, the FP8 format Sec. IV-C
+// evaluates); all sums and products are fp32 in both cases.
 //
 // Design for gfx950 (the paper's warp/block layout is prior art, not reused):
 //   * One wavefront owns one token at a time: its Q row and K row are spread
-//     over the 64 lanes in 16-byte chunks (8 bf16), chunk c on lane c % 64, so
-//     the row reduction needs no LDS and no barrier: four DPP row steps and
-//     four readlanes.
+//     over the 64 lanes in 16-byte chunks (8 bf16 or 16 fp8), chunk c on lane
+//     c % 64, so the row reduction needs no LDS and no barrier: four DPP row
+//     steps and four readlanes.
 //   * The rows stay in registers between Phase A and Phase C (one HBM read of
 //     x, one write of y); gamma is loaded into registers once per wavefront and
 //     reused for every token of the persistent loop.
@@ -51,8 +54,6 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
-constexpr int kChunk = 8;           // bf16 elements per 128-bit access
-constexpr int kMaxRegChunks = 8;    // chunks per lane held in registers (d_local <= 4096)
 constexpr int kMaxFastTp = kWave;   // one statistic slot per lane
 constexpr int kMaxStageBytes = 64 * 1024;
 // Grid sizing of the register path (measured on MI355X: HBM throughput peaks
@@ -65,15 +66,15 @@ constexpr int64_t kMinWavesPerCu = 6;
 enum Mode { kFused = 0, kApply = 1, kPartial = 2, kFusedWait = 3, kPublish = 4 };
 
 struct DevSeg {
-  const uint16_t* x;
+  const void* x;    // activations (element type set by the kernel's format)
   const float* w;
   float* partials;  // [tp * T], rank-major
-  uint16_t* y;
+  void* y;
   float* inv_rms;   // optional [T]
   int64_t ldx;
   int64_t ldy;
   int32_t d;        // d_local
-  int32_t nchunks;  // ceil(d_local / 8)
+  int32_t nchunks;  // ceil(d_local / elements per chunk)
   float d_full;     // divisor of the mean (H_total)
   int32_t vec;      // 128-bit accesses allowed
 };
@@ -110,15 +111,72 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return static_cast<uint16_t>(pack_bf16x2(f, 0.0f) & 0xffffu);
 }
 
-// Phase A on one 8-element chunk, ascending column order.
-__device__ __forceinline__ float chunk_sumsq(u32x4 v, float acc) {
+// Element formats. A 16-byte chunk holds kPer elements, element e of the chunk
+// at byte e * sizeof(Elem) (little-endian). Decoding is exact; encoding rounds
+// to nearest, ties to even.
+struct FmtBf16 {
+  using Elem = uint16_t;
+  static constexpr int kPer = 8;
+  __device__ static __forceinline__ void unpack(u32x4 v, float (&f)[8]) {
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const float a = bf16_lo(v[e]);
-    const float b = bf16_hi(v[e]);
-    acc = __builtin_fmaf(a, a, acc);
-    acc = __builtin_fmaf(b, b, acc);
+    for (int e = 0; e < 4; ++e) {
+      f[2 * e] = bf16_lo(v[e]);
+      f[2 * e + 1] = bf16_hi(v[e]);
+    }
   }
+  __device__ static __forceinline__ u32x4 pack(const float (&f)[8]) {
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(f[2 * e], f[2 * e + 1]);
+    return o;
+  }
+  __device__ static __forceinline__ float decode(Elem b) { return bf16_to_f32(b); }
+  __device__ static __forceinline__ Elem encode(float f) { return f32_to_bf16(f); }
+};
+
+// FP8-E4M3 (OCP e4m3fn) with the gfx950 conversions: v_cvt_pk_f32_fp8 decodes
+// two bytes of a word, v_cvt_pk_fp8_f32 rounds two floats to nearest even into
+// two bytes; a value that rounds beyond 448 becomes NaN (the format has no
+// infinity), as in the usual cast to e4m3fn.
+struct FmtFp8 {
+  using Elem = uint8_t;
+  static constexpr int kPer = 16;
+  __device__ static __forceinline__ void unpack(u32x4 v, float (&f)[16]) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(v[e]), false);
+      const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(v[e]), true);
+      f[4 * e] = lo[0];
+      f[4 * e + 1] = lo[1];
+      f[4 * e + 2] = hi[0];
+      f[4 * e + 3] = hi[1];
+    }
+  }
+  __device__ static __forceinline__ u32x4 pack(const float (&f)[16]) {
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      int w = __builtin_amdgcn_cvt_pk_fp8_f32(f[4 * e], f[4 * e + 1], 0, false);
+      w = __builtin_amdgcn_cvt_pk_fp8_f32(f[4 * e + 2], f[4 * e + 3], w, true);
+      o[e] = static_cast<uint32_t>(w);
+    }
+    return o;
+  }
+  __device__ static __forceinline__ float decode(Elem b) {
+    return __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(b), false)[0];
+  }
+  __device__ static __forceinline__ Elem encode(float f) {
+    return static_cast<Elem>(__builtin_amdgcn_cvt_pk_fp8_f32(f, 0.0f, 0, false) & 0xff);
+  }
+};
+
+// Phase A on one chunk, ascending column order.
+template <class F>
+__device__ __forceinline__ float chunk_sumsq(u32x4 v, float acc) {
+  float f[F::kPer];
+  F::unpack(v, f);
+#pragma unroll
+  for (int e = 0; e < F::kPer; ++e) acc = __builtin_fmaf(f[e], f[e], acc);
   return acc;
 }
 
@@ -241,23 +299,36 @@ __device__ __forceinline__ void st4f_lane0(float v, Rsrc r, int lane) {
                                         0);
 }
 
-template <int N>
+// gamma of a chunk: kPer floats, kPer / 4 float4 values.
+template <class F>
+constexpr int kGammaVecs = F::kPer / 4;
+
+template <class F, int N>
 __device__ __forceinline__ void load_gamma(const DevSeg& s, int64_t col, int lane,
-                                           f32x4 (&g)[N][2]) {
-  const Rsrc r = make_rsrc(s.w + col, static_cast<uint32_t>(s.nchunks) * 32u);
+                                           f32x4 (&g)[N][kGammaVecs<F>]) {
+  constexpr int kG = kGammaVecs<F>;
+  const Rsrc r = make_rsrc(s.w + col, static_cast<uint32_t>(s.nchunks) * (kG * 16u));
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     const int c = i * kWave + lane;
-    g[i][0] = __builtin_bit_cast(f32x4, ld16(r, c * 32));
-    g[i][1] = __builtin_bit_cast(f32x4, ld16(r, c * 32 + 16));
+#pragma unroll
+    for (int j = 0; j < kG; ++j) g[i][j] = __builtin_bit_cast(f32x4, ld16(r, (c * kG + j) * 16));
   }
 }
 
+// Address of element (t, col) of a row-major tensor with leading dimension ld.
+template <class F>
+__device__ __forceinline__ const typename F::Elem* elem_at(const void* base, int64_t t, int64_t ld,
+                                                           int64_t col) {
+  return static_cast<const typename F::Elem*>(base) + t * ld + col;
+}
+
 // `live` false: an empty descriptor -- every lane reads zeros, nothing is fetched.
-template <int N>
+template <class F, int N>
 __device__ __forceinline__ void load_row(const DevSeg& s, int64_t col, int64_t t, int lane,
                                          u32x4 (&x)[N], bool live = true) {
-  const Rsrc r = make_rsrc(s.x + t * s.ldx + col, live ? static_cast<uint32_t>(s.nchunks) * 16u : 0u);
+  const Rsrc r = make_rsrc(elem_at<F>(s.x, t, s.ldx, col),
+                           live ? static_cast<uint32_t>(s.nchunks) * 16u : 0u);
 #pragma unroll
   for (int i = 0; i < N; ++i) x[i] = ld16_nt(r, (i * kWave + lane) * 16);
 }
@@ -274,40 +345,38 @@ __device__ __forceinline__ float load_slots_buf(const float* partials, int64_t T
   return ld4f(r, off);
 }
 
-template <int N>
+template <class F, int N>
 __device__ __forceinline__ float row_lane_sumsq(const u32x4 (&x)[N]) {
   float acc = 0.0f;
 #pragma unroll
-  for (int i = 0; i < N; ++i) acc = chunk_sumsq(x[i], acc);
+  for (int i = 0; i < N; ++i) acc = chunk_sumsq<F>(x[i], acc);
   return acc;
 }
 
 // Phase B compute path: z = x * gamma, elementwise in fp32.
-template <int N>
-__device__ __forceinline__ void times_gamma(const u32x4 (&x)[N], const f32x4 (&g)[N][2],
-                                            float (&z)[N][8]) {
+template <class F, int N>
+__device__ __forceinline__ void times_gamma(const u32x4 (&x)[N], const f32x4 (&g)[N][kGammaVecs<F>],
+                                            float (&z)[N][F::kPer]) {
 #pragma unroll
   for (int i = 0; i < N; ++i) {
+    float f[F::kPer];
+    F::unpack(x[i], f);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const f32x4& gg = g[i][e >> 1];
-      z[i][2 * e] = bf16_lo(x[i][e]) * gg[(2 * e) & 3];
-      z[i][2 * e + 1] = bf16_hi(x[i][e]) * gg[(2 * e + 1) & 3];
-    }
+    for (int e = 0; e < F::kPer; ++e) z[i][e] = f[e] * g[i][e >> 2][e & 3];
   }
 }
 
-// Phase C: y = bf16(z * inv), non-temporal 128-bit stores.
-template <int N>
+// Phase C: y = round(z * inv), non-temporal 128-bit stores.
+template <class F, int N>
 __device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t col, int64_t t, int lane,
-                                             const float (&z)[N][8], float inv) {
-  const Rsrc r = make_rsrc(s.y + t * s.ldy + col, static_cast<uint32_t>(s.nchunks) * 16u);
+                                             const float (&z)[N][F::kPer], float inv) {
+  const Rsrc r = make_rsrc(elem_at<F>(s.y, t, s.ldy, col), static_cast<uint32_t>(s.nchunks) * 16u);
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    u32x4 o;
+    float o[F::kPer];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(z[i][2 * e] * inv, z[i][2 * e + 1] * inv);
-    st16_nt(o, r, (i * kWave + lane) * 16);
+    for (int e = 0; e < F::kPer; ++e) o[e] = z[i][e] * inv;
+    st16_nt(F::pack(o), r, (i * kWave + lane) * 16);
   }
 }
 
@@ -388,13 +457,13 @@ struct TokenRegs {
 };
 
 // `live` false (a pipelined request past the last token): nothing is fetched.
-template <int N0, int N1, int MODE>
+template <class F, int N0, int N1, int MODE>
 __device__ __forceinline__ void fetch_token(const KParams& p, const WaveSlice& ws, int64_t t,
                                             int lane, int own_rank,
                                             TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
                                             bool live = true) {
-  load_row<N0>(p.seg[0], ws.col0, t, lane, r.x0, live);
-  if constexpr (N1 > 0) load_row<N1>(p.seg[1], ws.col1, t, lane, r.x1, live);
+  load_row<F, N0>(p.seg[0], ws.col0, t, lane, r.x0, live);
+  if constexpr (N1 > 0) load_row<F, N1>(p.seg[1], ws.col1, t, lane, r.x1, live);
   r.slots0 = 0.0f;
   r.slots1 = 0.0f;
   if constexpr (MODE == kFused || MODE == kApply) {
@@ -411,10 +480,11 @@ __device__ __forceinline__ void fetch_token(const KParams& p, const WaveSlice& w
 }
 
 // Phases A, B and C of token t, whose rows and slots are in `r`.
-template <int N0, int N1, int MODE>
+template <class F, int N0, int N1, int MODE>
 __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice& ws, int64_t t,
-                                              int lane, int own_rank, const f32x4 (&g0)[N0][2],
-                                              const f32x4 (&g1)[(N1 > 0 ? N1 : 1)][2],
+                                              int lane, int own_rank,
+                                              const f32x4 (&g0)[N0][kGammaVecs<F>],
+                                              const f32x4 (&g1)[(N1 > 0 ? N1 : 1)][kGammaVecs<F>],
                                               const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
                                               bool& given_up) {
   constexpr int M1 = N1 > 0 ? N1 : 1;
@@ -424,8 +494,8 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
   // Phase A: per-lane partial sums (not needed when every slot is given).
   float a0 = 0.0f, a1 = 0.0f;
   if constexpr (MODE != kApply) {
-    a0 = row_lane_sumsq<N0>(r.x0);
-    if constexpr (N1 > 0) a1 = row_lane_sumsq<N1>(r.x1);
+    a0 = row_lane_sumsq<F, N0>(r.x0);
+    if constexpr (N1 > 0) a1 = row_lane_sumsq<F, N1>(r.x1);
   }
 
   if constexpr (MODE == kPartial) {
@@ -450,10 +520,10 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
     }
 
     // Phase B, compute path: independent of the statistic.
-    float z0[N0][8];
-    float z1[M1][8];
-    times_gamma<N0>(r.x0, g0, z0);
-    if constexpr (N1 > 0) times_gamma<N1>(r.x1, g1, z1);
+    float z0[N0][F::kPer];
+    float z1[M1][F::kPer];
+    times_gamma<F, N0>(r.x0, g0, z0);
+    if constexpr (N1 > 0) times_gamma<F, N1>(r.x1, g1, z1);
 
     // Phase B, reduction path.
     float slots0 = r.slots0, slots1 = r.slots1;
@@ -479,8 +549,8 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
     }
 
     // Phase C.
-    store_scaled<N0>(s0, ws.col0, t, lane, z0, inv0);
-    if constexpr (N1 > 0) store_scaled<N1>(s1, ws.col1, t, lane, z1, inv1);
+    store_scaled<F, N0>(s0, ws.col0, t, lane, z0, inv0);
+    if constexpr (N1 > 0) store_scaled<F, N1>(s1, ws.col1, t, lane, z1, inv1);
     const int64_t own_slot = (static_cast<int64_t>(ws.rank) * p.T + t) * 4;
     if constexpr (MODE == kFused) {
       st4f_lane0(own0, make_rsrc_at(s0.partials, own_slot, 4u), lane);
@@ -498,7 +568,7 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
 // alternate roles (the loop is unrolled by two) so that no copy forces a wait
 // on the requests in flight; past the last token the request goes through an
 // empty descriptor, so it is unconditional and fetches nothing.
-template <int N0, int N1, int MODE, int SCHED>
+template <class F, int N0, int N1, int MODE, int SCHED>
 __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
   constexpr bool PF = (SCHED == 1);
   constexpr int M1 = N1 > 0 ? N1 : 1;
@@ -531,36 +601,36 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
   }
   if (t >= end) return;
 
-  f32x4 g0[N0][2];
-  f32x4 g1[M1][2];
+  f32x4 g0[N0][kGammaVecs<F>];
+  f32x4 g1[M1][kGammaVecs<F>];
   if constexpr (MODE != kPartial && MODE != kPublish) {
-    load_gamma<N0>(p.seg[0], ws.col0, lane, g0);
-    if constexpr (N1 > 0) load_gamma<N1>(p.seg[1], ws.col1, lane, g1);
+    load_gamma<F, N0>(p.seg[0], ws.col0, lane, g0);
+    if constexpr (N1 > 0) load_gamma<F, N1>(p.seg[1], ws.col1, lane, g1);
   }
 
   TokenRegs<N0, M1> ra;
-  fetch_token<N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
+  fetch_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
   if constexpr (PF) {
     TokenRegs<N0, M1> rb;
     const int64_t last = end - 1;
     while (true) {
       int64_t tn = t + step;
-      fetch_token<N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, rb, tn <= last);
-      process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
+      fetch_token<F, N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, rb, tn <= last);
+      process_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
       if (tn > last) break;
       t = tn;
       tn = t + step;
-      fetch_token<N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, ra, tn <= last);
-      process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, rb, given_up);
+      fetch_token<F, N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, ra, tn <= last);
+      process_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, rb, given_up);
       if (tn > last) break;
       t = tn;
     }
   } else {
     while (true) {
-      process_token<N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
+      process_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
       t += step;
       if (t >= end) break;
-      fetch_token<N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
+      fetch_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
     }
   }
 }
@@ -575,28 +645,37 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
 // (x * gamma) * factor -- the same operations, order and reduction tree as
 // every other path.
 
-// Phase C of one wide row from gamma in LDS: y = bf16((x * gamma) * inv).
-template <int N>
+// Phase C of one chunk: y = round((x * gamma) * inv), gamma from kGammaVecs<F> vectors.
+template <class F>
+__device__ __forceinline__ u32x4 scale_chunk(u32x4 v, const f32x4* g, float inv) {
+  constexpr int kG = kGammaVecs<F>;
+  f32x4 gq[kG];
+#pragma unroll
+  for (int j = 0; j < kG; ++j) gq[j] = g[j];
+  float f[F::kPer];
+  F::unpack(v, f);
+  float o[F::kPer];
+#pragma unroll
+  for (int e = 0; e < F::kPer; ++e) o[e] = (f[e] * gq[e >> 2][e & 3]) * inv;
+  return F::pack(o);
+}
+
+// Phase C of one wide row from gamma in LDS.
+template <class F, int N>
 __device__ __forceinline__ void store_scaled_lds(const DevSeg& s, int64_t t, int lane,
                                                  const u32x4 (&x)[N], const f32x4* g, float inv) {
-  const Rsrc ry = make_rsrc(s.y + t * s.ldy, static_cast<uint32_t>(s.nchunks) * 16u);
+  const Rsrc ry = make_rsrc(elem_at<F>(s.y, t, s.ldy, 0), static_cast<uint32_t>(s.nchunks) * 16u);
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     const int c = i * kWave + lane;
     const int cc = c < s.nchunks ? c : 0;  // masked lanes: any in-range gamma, store dropped
-    const f32x4 ga = g[2 * cc], gb = g[2 * cc + 1];
-    u32x4 o;
-    o[0] = pack_bf16x2((bf16_lo(x[i][0]) * ga[0]) * inv, (bf16_hi(x[i][0]) * ga[1]) * inv);
-    o[1] = pack_bf16x2((bf16_lo(x[i][1]) * ga[2]) * inv, (bf16_hi(x[i][1]) * ga[3]) * inv);
-    o[2] = pack_bf16x2((bf16_lo(x[i][2]) * gb[0]) * inv, (bf16_hi(x[i][2]) * gb[1]) * inv);
-    o[3] = pack_bf16x2((bf16_lo(x[i][3]) * gb[2]) * inv, (bf16_hi(x[i][3]) * gb[3]) * inv);
-    st16_nt(o, ry, c * 16);
+    st16_nt(scale_chunk<F>(x[i], g + kGammaVecs<F> * cc, inv), ry, c * 16);
     // keep the scheduler from hoisting every chunk's gamma reads (register pressure)
     if ((i & 1) == 1) __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-template <int N0, int N1, int MODE>
+template <class F, int N0, int N1, int MODE>
 __global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
   extern __shared__ __align__(16) float gamma_lds[];  // [d0 + d1] (fused / apply)
   constexpr int M1 = N1 > 0 ? N1 : 1;
@@ -623,8 +702,8 @@ __global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
   for (int64_t t = wave_index(); t < p.T; t += nwaves) {
     u32x4 x0[N0];
     u32x4 x1[M1];
-    load_row<N0>(s0, 0, t, lane, x0);
-    if constexpr (N1 > 0) load_row<N1>(s1, 0, t, lane, x1);
+    load_row<F, N0>(s0, 0, t, lane, x0);
+    if constexpr (N1 > 0) load_row<F, N1>(s1, 0, t, lane, x1);
     float sl0 = 0.0f, sl1 = 0.0f;
     if constexpr (MODE != kPartial) {
       sl0 = load_slots_buf(s0.partials, p.T, t, lane, p.tp, own_rank);
@@ -632,8 +711,8 @@ __global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
     }
     float own0 = 0.0f, own1 = 0.0f;
     if constexpr (MODE != kApply) {
-      own0 = wave_sum(row_lane_sumsq<N0>(x0));
-      if constexpr (N1 > 0) own1 = wave_sum(row_lane_sumsq<N1>(x1));
+      own0 = wave_sum(row_lane_sumsq<F, N0>(x0));
+      if constexpr (N1 > 0) own1 = wave_sum(row_lane_sumsq<F, N1>(x1));
     }
     if constexpr (MODE == kPartial) {
       st4f_lane0(own0, make_rsrc_at(s0.partials, t * 4, 4u), lane);
@@ -648,8 +727,8 @@ __global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
       for (int i = 0; i < N0; ++i) asm volatile("" : "+v"(x0[i]));
 #pragma unroll
       for (int i = 0; i < M1; ++i) asm volatile("" : "+v"(x1[i]));
-      store_scaled_lds<N0>(s0, t, lane, x0, g0, inv0);
-      if constexpr (N1 > 0) store_scaled_lds<N1>(s1, t, lane, x1, g1, inv1);
+      store_scaled_lds<F, N0>(s0, t, lane, x0, g0, inv0);
+      if constexpr (N1 > 0) store_scaled_lds<F, N1>(s1, t, lane, x1, g1, inv1);
       const int64_t own_slot = (static_cast<int64_t>(p.rank) * p.T + t) * 4;
       if constexpr (MODE == kFused) {
         st4f_lane0(own0, make_rsrc_at(s0.partials, own_slot, 4u), lane);
@@ -668,9 +747,12 @@ __global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
 // The row is staged in LDS between Phase A and Phase C when it fits; each lane
 // reads back only the chunks it wrote, so no barrier is needed.
 
-template <int MODE>
+template <class F, int MODE>
 __global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage_elems) {
-  extern __shared__ __align__(16) uint16_t stage[];
+  using E = typename F::Elem;
+  constexpr int kPer = F::kPer;
+  extern __shared__ __align__(16) unsigned char stage_raw[];
+  E* const stage = reinterpret_cast<E*>(stage_raw);
   const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
   const int64_t nwaves = gridDim.x;
   const int own_rank = (MODE == kFused) ? p.rank : -1;
@@ -678,8 +760,8 @@ __global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage
   for (int64_t t = wave_index(); t < p.T; t += nwaves) {
     for (int si = 0; si < p.nseg; ++si) {
       const DevSeg& s = p.seg[si];
-      const uint16_t* xrow = s.x + t * s.ldx;
-      const bool staged = (MODE == kFused) && (s.nchunks * kChunk <= stage_elems);
+      const E* xrow = elem_at<F>(s.x, t, s.ldx, 0);
+      const bool staged = (MODE == kFused) && (s.nchunks * kPer <= stage_elems);
 
       float own = 0.0f;
       if constexpr (MODE != kApply) {
@@ -687,14 +769,14 @@ __global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage
         for (int c = lane; c < s.nchunks; c += kWave) {
           if (s.vec) {
             const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(xrow) + c);
-            a = chunk_sumsq(v, a);
-            if (staged) *reinterpret_cast<u32x4*>(stage + c * kChunk) = v;
+            a = chunk_sumsq<F>(v, a);
+            if (staged) *reinterpret_cast<u32x4*>(stage + c * kPer) = v;
           } else {
-            for (int e = 0; e < kChunk; ++e) {
-              const int j = c * kChunk + e;
+            for (int e = 0; e < kPer; ++e) {
+              const int j = c * kPer + e;
               if (j < s.d) {
-                const uint16_t b = xrow[j];
-                const float f = bf16_to_f32(b);
+                const E b = xrow[j];
+                const float f = F::decode(b);
                 a = __builtin_fmaf(f, f, a);
                 if (staged) stage[j] = b;
               }
@@ -719,27 +801,22 @@ __global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage
         }
         const float inv = rms_inverse(S, s.d_full, p.eps);
 
-        uint16_t* yrow = s.y + t * s.ldy;
+        E* yrow = const_cast<E*>(elem_at<F>(s.y, t, s.ldy, 0));
         for (int c = lane; c < s.nchunks; c += kWave) {
           if (s.vec) {
-            const u32x4 v = staged ? *reinterpret_cast<const u32x4*>(stage + c * kChunk)
+            const u32x4 v = staged ? *reinterpret_cast<const u32x4*>(stage + c * kPer)
                                    : __builtin_nontemporal_load(
                                          reinterpret_cast<const u32x4*>(xrow) + c);
-            const f32x4* gp = reinterpret_cast<const f32x4*>(s.w) + 2 * c;
-            const f32x4 ga = gp[0], gb = gp[1];
-            u32x4 o;
-            o[0] = pack_bf16x2((bf16_lo(v[0]) * ga[0]) * inv, (bf16_hi(v[0]) * ga[1]) * inv);
-            o[1] = pack_bf16x2((bf16_lo(v[1]) * ga[2]) * inv, (bf16_hi(v[1]) * ga[3]) * inv);
-            o[2] = pack_bf16x2((bf16_lo(v[2]) * gb[0]) * inv, (bf16_hi(v[2]) * gb[1]) * inv);
-            o[3] = pack_bf16x2((bf16_lo(v[3]) * gb[2]) * inv, (bf16_hi(v[3]) * gb[3]) * inv);
-            __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(yrow) + c);
+            const f32x4* gp = reinterpret_cast<const f32x4*>(s.w) + kGammaVecs<F> * c;
+            __builtin_nontemporal_store(scale_chunk<F>(v, gp, inv),
+                                        reinterpret_cast<u32x4*>(yrow) + c);
           } else {
-            for (int e = 0; e < kChunk; ++e) {
-              const int j = c * kChunk + e;
+            for (int e = 0; e < kPer; ++e) {
+              const int j = c * kPer + e;
               if (j < s.d) {
-                const uint16_t b = staged ? stage[j] : xrow[j];
-                const float z = bf16_to_f32(b) * s.w[j];
-                yrow[j] = f32_to_bf16(z * inv);
+                const E b = staged ? stage[j] : xrow[j];
+                const float z = F::decode(b) * s.w[j];
+                yrow[j] = F::encode(z * inv);
               }
             }
           }
@@ -760,68 +837,111 @@ __global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage
 typedef void (*RowsFn)(KParams);
 typedef void (*GenericFn)(KParams, int32_t);
 
+enum Format { kBf16 = 0, kFp8 = 1 };
+
+// Per-format limits of the specialised kernels. The register path keeps, per
+// chunk and lane, the packed row, its fp32 products with gamma and gamma
+// itself: 8 bf16 chunks (d_local <= 4096) or 4 fp8 chunks (d_local <= 4096)
+// per tensor take the same registers. The wide path keeps only the packed rows
+// (slot 0 up to 32 bf16 / 16 fp8 chunks per lane, slot 1 as the register path).
+struct FormatInfo {
+  int esz;             // bytes per element
+  int per;             // elements per 16-byte chunk
+  int reg_max;         // register path: chunks per lane
+  int wide_n0[2];      // wide path: chunks per lane of the kernels for slot 0
+  const char* suffix;  // kernel-family suffix in launch names
+};
+constexpr FormatInfo kFormat[2] = {{2, 8, 8, {16, 32}, ""}, {1, 16, 4, {8, 16}, "_fp8"}};
+
 // Chunks per lane are rounded up to 1, 2, 4 or 8; unused chunks are masked.
 constexpr int kNIdx[9] = {-1, 0, 1, 2, 2, 3, 3, 3, 3};  // chunks/lane -> table index
 constexpr int kNVal[4] = {1, 2, 4, 8};
 
-#define QKN_ROW_SET(M, A, S)                                                           \
-  {qkn_rows<A, 0, M, S>, qkn_rows<A, 1, M, S>, qkn_rows<A, 2, M, S>, qkn_rows<A, 4, M, S>, \
-   qkn_rows<A, 8, M, S>}
-#define QKN_ONE_SET(M, S) \
-  {qkn_rows<1, 0, M, S>, qkn_rows<2, 0, M, S>, qkn_rows<4, 0, M, S>, qkn_rows<8, 0, M, S>}
-#define QKN_FULL_SET(M, S) \
-  {QKN_ROW_SET(M, 1, S), QKN_ROW_SET(M, 2, S), QKN_ROW_SET(M, 4, S), QKN_ROW_SET(M, 8, S)}
+#define QKN_ROW_SET(F, M, A, S)                                                     \
+  {qkn_rows<F, A, 0, M, S>, qkn_rows<F, A, 1, M, S>, qkn_rows<F, A, 2, M, S>,       \
+   qkn_rows<F, A, 4, M, S>, qkn_rows<F, A, 8, M, S>}
+#define QKN_ONE_SET(F, M, S) \
+  {qkn_rows<F, 1, 0, M, S>, qkn_rows<F, 2, 0, M, S>, qkn_rows<F, 4, 0, M, S>, qkn_rows<F, 8, 0, M, S>}
+#define QKN_FULL_SET(F, M, S) \
+  {QKN_ROW_SET(F, M, 1, S), QKN_ROW_SET(F, M, 2, S), QKN_ROW_SET(F, M, 4, S), QKN_ROW_SET(F, M, 8, S)}
+// fp8: up to 4 chunks per lane, one token per step
+#define QKN_ROW_SET8(M, A)                                                                     \
+  {qkn_rows<FmtFp8, A, 0, M, 0>, qkn_rows<FmtFp8, A, 1, M, 0>, qkn_rows<FmtFp8, A, 2, M, 0>, \
+   qkn_rows<FmtFp8, A, 4, M, 0>, nullptr}
+#define QKN_FULL_SET8(M) \
+  {QKN_ROW_SET8(M, 1), QKN_ROW_SET8(M, 2), QKN_ROW_SET8(M, 4), {nullptr, nullptr, nullptr, nullptr, nullptr}}
+#define QKN_ONE_SET8(M) \
+  {qkn_rows<FmtFp8, 1, 0, M, 0>, qkn_rows<FmtFp8, 2, 0, M, 0>, qkn_rows<FmtFp8, 4, 0, M, 0>, nullptr}
 
 // Schedules: 0 one token per step, 1 pipelined (next token requested early).
 // [schedule][N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
-const RowsFn kFusedTable[2][4][5] = {QKN_FULL_SET(kFused, 0), QKN_FULL_SET(kFused, 1)};
-const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(kApply, 0), QKN_ONE_SET(kApply, 1)};
-const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(kPartial, 0), QKN_ONE_SET(kPartial, 1)};
-const RowsFn kFusedWaitTable[2][4][5] = {QKN_FULL_SET(kFusedWait, 0),
-                                         QKN_FULL_SET(kFusedWait, 1)};
-const RowsFn kPublishTable[4] = QKN_ONE_SET(kPublish, 0);
-const GenericFn kGenericTable[3] = {qkn_generic<kFused>, qkn_generic<kApply>,
-                                    qkn_generic<kPartial>};
-constexpr int kMaxWideChunks = 32;  // chunks per lane on the wide path (d_local <= 16384)
+const RowsFn kFusedTable[2][4][5] = {QKN_FULL_SET(FmtBf16, kFused, 0),
+                                     QKN_FULL_SET(FmtBf16, kFused, 1)};
+const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(FmtBf16, kApply, 0), QKN_ONE_SET(FmtBf16, kApply, 1)};
+const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(FmtBf16, kPartial, 0),
+                                    QKN_ONE_SET(FmtBf16, kPartial, 1)};
+const RowsFn kFusedWaitTable[2][4][5] = {QKN_FULL_SET(FmtBf16, kFusedWait, 0),
+                                         QKN_FULL_SET(FmtBf16, kFusedWait, 1)};
+const RowsFn kPublishTable[4] = QKN_ONE_SET(FmtBf16, kPublish, 0);
+// fp8: [N0 index][N1 index]
+const RowsFn kFusedTable8[4][5] = QKN_FULL_SET8(kFused);
+const RowsFn kApplyTable8[4] = QKN_ONE_SET8(kApply);
+const RowsFn kPartialTable8[4] = QKN_ONE_SET8(kPartial);
+const GenericFn kGenericTable[2][3] = {
+    {qkn_generic<FmtBf16, kFused>, qkn_generic<FmtBf16, kApply>, qkn_generic<FmtBf16, kPartial>},
+    {qkn_generic<FmtFp8, kFused>, qkn_generic<FmtFp8, kApply>, qkn_generic<FmtFp8, kPartial>}};
 constexpr int kMaxWideLdsBytes = 64 * 1024;
-#define QKN_WIDE_SET(A, M) \
-  {qkn_wide<A, 0, M>, qkn_wide<A, 1, M>, qkn_wide<A, 2, M>, qkn_wide<A, 4, M>, qkn_wide<A, 8, M>}
-// [wide N0: 16, 32][mode][N1 index: 0 = single segment, then 1, 2, 4, 8]
-const RowsFn kWideTable[2][3][5] = {
-    {QKN_WIDE_SET(16, kFused), QKN_WIDE_SET(16, kApply), QKN_WIDE_SET(16, kPartial)},
-    {QKN_WIDE_SET(32, kFused), QKN_WIDE_SET(32, kApply), QKN_WIDE_SET(32, kPartial)}};
+#define QKN_WIDE_SET(F, A, M)                                                            \
+  {qkn_wide<F, A, 0, M>, qkn_wide<F, A, 1, M>, qkn_wide<F, A, 2, M>, qkn_wide<F, A, 4, M>, \
+   qkn_wide<F, A, 8, M>}
+#define QKN_WIDE_SET8(A, M)                                                                    \
+  {qkn_wide<FmtFp8, A, 0, M>, qkn_wide<FmtFp8, A, 1, M>, qkn_wide<FmtFp8, A, 2, M>,           \
+   qkn_wide<FmtFp8, A, 4, M>, nullptr}
+// [format][wide N0 index][mode][N1 index: 0 = single segment, then 1, 2, 4, 8]
+const RowsFn kWideTable[2][2][3][5] = {
+    {{QKN_WIDE_SET(FmtBf16, 16, kFused), QKN_WIDE_SET(FmtBf16, 16, kApply),
+      QKN_WIDE_SET(FmtBf16, 16, kPartial)},
+     {QKN_WIDE_SET(FmtBf16, 32, kFused), QKN_WIDE_SET(FmtBf16, 32, kApply),
+      QKN_WIDE_SET(FmtBf16, 32, kPartial)}},
+    {{QKN_WIDE_SET8(8, kFused), QKN_WIDE_SET8(8, kApply), QKN_WIDE_SET8(8, kPartial)},
+     {QKN_WIDE_SET8(16, kFused), QKN_WIDE_SET8(16, kApply), QKN_WIDE_SET8(16, kPartial)}}};
 
 const char* const kModeName[5] = {"fused", "apply", "partial", "fused_wait", "publish"};
 
-// Static names "rows<N0,N1>/mode" ("rows_pf<...>" when pipelined).
-const char* rows_name(int mode, int sched, int i0, int i1) {
-  static char names[5][2][4][5][40];
+// Static names "rows<N0,N1>/mode" ("rows_pf<...>" when pipelined, "rows_fp8<...>" for fp8).
+const char* rows_name(int fmt, int mode, int sched, int i0, int i1) {
+  static char names[2][5][2][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
-    const char* const prefix[2] = {"rows", "rows_pf"};
-    for (int m = 0; m < 5; ++m)
-      for (int f = 0; f < 2; ++f)
-        for (int a = 0; a < 4; ++a)
-          for (int b = 0; b < 5; ++b)
-            snprintf(names[m][f][a][b], sizeof(names[m][f][a][b]), "%s<%d,%d>/%s", prefix[f],
-                     kNVal[a], b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
+    const char* const prefix[2][2] = {{"rows", "rows_pf"}, {"rows_fp8", "rows_pf_fp8"}};
+    for (int fm = 0; fm < 2; ++fm)
+      for (int m = 0; m < 5; ++m)
+        for (int f = 0; f < 2; ++f)
+          for (int a = 0; a < 4; ++a)
+            for (int b = 0; b < 5; ++b)
+              snprintf(names[fm][m][f][a][b], sizeof(names[fm][m][f][a][b]), "%s<%d,%d>/%s",
+                       prefix[fm][f], kNVal[a], b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
   });
-  return names[mode][sched][i0][i1];
+  return names[fmt][mode][sched][i0][i1];
 }
-const char* const kGenericName[3] = {"generic/fused", "generic/apply", "generic/partial"};
+const char* const kGenericName[2][3] = {{"generic/fused", "generic/apply", "generic/partial"},
+                                        {"generic_fp8/fused", "generic_fp8/apply",
+                                         "generic_fp8/partial"}};
 
-// Static names "wide<N0,N1>/mode".
-const char* wide_name(int mode, int i0, int i1) {
-  static char names[3][2][5][40];
+// Static names "wide<N0,N1>/mode" ("wide_fp8<...>" for fp8).
+const char* wide_name(int fmt, int mode, int i0, int i1) {
+  static char names[2][3][2][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
-    for (int m = 0; m < 3; ++m)
-      for (int a = 0; a < 2; ++a)
-        for (int b = 0; b < 5; ++b)
-          snprintf(names[m][a][b], sizeof(names[m][a][b]), "wide<%d,%d>/%s", a ? 32 : 16,
-                   b == 0 ? 0 : kNVal[b - 1], kModeName[m]);
+    for (int fm = 0; fm < 2; ++fm)
+      for (int m = 0; m < 3; ++m)
+        for (int a = 0; a < 2; ++a)
+          for (int b = 0; b < 5; ++b)
+            snprintf(names[fm][m][a][b], sizeof(names[fm][m][a][b]), "wide%s<%d,%d>/%s",
+                     kFormat[fm].suffix, kFormat[fm].wide_n0[a], b == 0 ? 0 : kNVal[b - 1],
+                     kModeName[m]);
   });
-  return names[mode][i0][i1];
+  return names[fmt][mode][i0][i1];
 }
 
 // Options.
@@ -885,6 +1005,24 @@ int blocks_per_cu(int dev, const void* fn, int block, int lds, int* out) {
 
 // ---------------------------------------------------------------- validation
 
+// Host view of a segment of either format (qkn_seg or qkn_seg8).
+struct HSeg {
+  const void* x;
+  int64_t ldx;
+  const float* w;
+  float* partials;
+  void* y;
+  int64_t ldy;
+  float* inv_rms;
+  int64_t d_local;
+  int64_t d_full;
+};
+
+template <class S>
+HSeg to_hseg(const S& s) {
+  return HSeg{s.x, s.ldx, s.w, s.partials, s.y, s.ldy, s.inv_rms, s.d_local, s.d_full};
+}
+
 bool bad_eps(float eps) { return !(eps >= 0.0f) || !isfinite(eps); }
 
 // A strided byte region: `rows` rows of `width` elements every `ld` elements.
@@ -921,8 +1059,8 @@ bool spans_overlap(const Span& a, const Span& b) {
   return true;  // conservative
 }
 
-Span bf16_span(const void* p, int64_t rows, int64_t ld, int64_t width) {
-  return Span{reinterpret_cast<uintptr_t>(p), rows, ld, width, 2};
+Span elem_span(const void* p, int64_t rows, int64_t ld, int64_t width, int esz) {
+  return Span{reinterpret_cast<uintptr_t>(p), rows, ld, width, esz};
 }
 Span f32_span(const void* p, int64_t n) {
   return Span{reinterpret_cast<uintptr_t>(p), 1, n, n, 4};
@@ -932,12 +1070,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 constexpr int64_t kMaxWidth = (int64_t{1} << 30);  // d_local and strides fit in int32 chunk math
 
-struct Planned {
-  KParams kp;
-  int mode;
-};
-
-int check_seg_shape(const qkn_seg& s, int mode) {
+int check_seg_shape(const HSeg& s, int mode) {
   if (!s.x) return QKN_EINVAL;
   if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local) return QKN_EINVAL;
   if (mode != kPartial && mode != kPublish) {
@@ -950,7 +1083,7 @@ int check_seg_shape(const qkn_seg& s, int mode) {
 // Overlap rules: outputs (y, own statistic slots, inv_rms) may not overlap any
 // input or another output, except y == x with equal strides (in place) and a
 // segment's own slots inside its own partials array.
-int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, int mode,
+int check_overlaps(const HSeg* segs, int nseg, int tp, int rank, int64_t T, int mode, int esz,
                    const Span* extra = nullptr, int nextra = 0) {
   struct Item {
     Span s;
@@ -962,8 +1095,8 @@ int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, i
   int n = 0;
   for (int i = 0; i < nextra; ++i) items[n++] = Item{extra[i], true, 100 + i, 6};
   for (int i = 0; i < nseg; ++i) {
-    const qkn_seg& s = segs[i];
-    items[n++] = Item{bf16_span(s.x, T, s.ldx, s.d_local), false, i, 0};
+    const HSeg& s = segs[i];
+    items[n++] = Item{elem_span(s.x, T, s.ldx, s.d_local, esz), false, i, 0};
     if (mode == kPartial) {
       items[n++] = Item{f32_span(s.partials, T), true, i, 4};
       continue;
@@ -974,7 +1107,7 @@ int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, i
       if (mode == kApply || tp > 1) items[n++] = Item{f32_span(s.partials, tp * T), false, i, 2};
       if (mode == kFused) items[n++] = Item{f32_span(s.partials + (int64_t)rank * T, T), true, i, 4};
     }
-    items[n++] = Item{bf16_span(s.y, T, s.ldy, s.d_local), true, i, 3};
+    items[n++] = Item{elem_span(s.y, T, s.ldy, s.d_local, esz), true, i, 3};
     if (s.inv_rms) items[n++] = Item{f32_span(s.inv_rms, T), true, i, 5};
   }
   for (int a = 0; a < n; ++a) {
@@ -994,15 +1127,15 @@ int check_overlaps(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, i
   return QKN_OK;
 }
 
-bool seg_vec_ok(const qkn_seg& s, int mode) {
-  if (!aligned16(s.x) || (s.ldx % kChunk) || (s.d_local % kChunk)) return false;
+bool seg_vec_ok(const HSeg& s, int mode, int per) {
+  if (!aligned16(s.x) || (s.ldx % per) || (s.d_local % per)) return false;
   if (mode != kPartial && mode != kPublish) {
-    if (!aligned16(s.y) || !aligned16(s.w) || (s.ldy % kChunk)) return false;
+    if (!aligned16(s.y) || !aligned16(s.w) || (s.ldy % per)) return false;
   }
   return true;
 }
 
-DevSeg to_dev(const qkn_seg& s, int mode) {
+DevSeg to_dev(const HSeg& s, int mode, const FormatInfo& fi) {
   DevSeg d;
   d.x = s.x;
   d.w = s.w;
@@ -1012,9 +1145,9 @@ DevSeg to_dev(const qkn_seg& s, int mode) {
   d.ldx = s.ldx;
   d.ldy = (mode == kPartial || mode == kPublish) ? 0 : s.ldy;
   d.d = static_cast<int32_t>(s.d_local);
-  d.nchunks = static_cast<int32_t>((s.d_local + kChunk - 1) / kChunk);
+  d.nchunks = static_cast<int32_t>((s.d_local + fi.per - 1) / fi.per);
   d.d_full = static_cast<float>((mode == kPartial || mode == kPublish) ? s.d_local : s.d_full);
-  d.vec = seg_vec_ok(s, mode) ? 1 : 0;
+  d.vec = seg_vec_ok(s, mode, fi.per) ? 1 : 0;
   return d;
 }
 
@@ -1028,8 +1161,9 @@ struct WaitArgs {
   int group;        // > 1: every rank of the group in this launch
 };
 
-int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps, int mode,
+int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, int mode, int fmt,
            void* stream, const WaitArgs* wa = nullptr) {
+  const FormatInfo& fi = kFormat[fmt];
   KParams kp;
   memset(&kp, 0, sizeof(kp));
   kp.T = T;
@@ -1038,6 +1172,7 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   kp.rank = rank;
   kp.eps = eps;
   const bool waits = (mode == kFusedWait || mode == kPublish);
+  if (waits && fmt != kBf16) return QKN_ENOTSUP;
   if (waits) {
     kp.slots[0] = wa->slots[0];
     kp.slots[1] = wa->slots[1];
@@ -1052,33 +1187,32 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   bool fast = buffer_ok;
   bool wide = buffer_ok && !waits;
   int idx[2] = {0, 0};
-  int max_chunks = 0, max_per_lane = 0;
+  int max_chunks = 0;
   int64_t gamma_floats = 0;
   for (int i = 0; i < nseg; ++i) {
-    kp.seg[i] = to_dev(segs[i], mode);
+    kp.seg[i] = to_dev(segs[i], mode, fi);
     const int per_lane = (kp.seg[i].nchunks + kWave - 1) / kWave;
-    if (!kp.seg[i].vec || per_lane > kMaxRegChunks) fast = false;
+    if (!kp.seg[i].vec || per_lane > fi.reg_max) fast = false;
     else idx[i] = kNIdx[per_lane];
-    if (!kp.seg[i].vec || per_lane > kMaxWideChunks) wide = false;
+    if (!kp.seg[i].vec || per_lane > fi.wide_n0[1]) wide = false;
     if (kp.seg[i].nchunks > max_chunks) max_chunks = kp.seg[i].nchunks;
-    if (per_lane > max_per_lane) max_per_lane = per_lane;
     gamma_floats += kp.seg[i].d;
   }
   if (fast) wide = false;
   if (mode != kPartial && gamma_floats * 4 > kMaxWideLdsBytes) wide = false;
   int wide_i0 = 0, wide_i1 = 0;
   if (wide) {
-    // the wider tensor goes first (slot 0 holds up to 32 chunks per lane, slot 1 up to 8)
+    // the wider tensor goes first (slot 0 takes the wide row, slot 1 a register-path one)
     if (nseg == 2 && kp.seg[1].nchunks > kp.seg[0].nchunks) {
       const DevSeg tmp = kp.seg[0];
       kp.seg[0] = kp.seg[1];
       kp.seg[1] = tmp;
     }
     const int pl0 = (kp.seg[0].nchunks + kWave - 1) / kWave;
-    wide_i0 = pl0 <= 16 ? 0 : 1;
+    wide_i0 = pl0 <= fi.wide_n0[0] ? 0 : 1;
     if (nseg == 2) {
       const int pl1 = (kp.seg[1].nchunks + kWave - 1) / kWave;
-      if (pl1 > kMaxRegChunks) wide = false;  // both tensors wide: general path
+      if (pl1 > fi.reg_max) wide = false;  // both tensors wide: general path
       else wide_i1 = kNIdx[pl1] + 1;
     }
   }
@@ -1088,29 +1222,37 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   const char* name;
   int lds = 0;
   int32_t stage_elems = 0;
+  const int i1 = nseg == 2 ? idx[1] + 1 : 0;
   if (wide) {
-    fn = reinterpret_cast<const void*>(kWideTable[wide_i0][mode][wide_i1]);
-    name = wide_name(mode, wide_i0, wide_i1);
+    fn = reinterpret_cast<const void*>(kWideTable[fmt][wide_i0][mode][wide_i1]);
+    name = wide_name(fmt, mode, wide_i0, wide_i1);
     lds = (mode == kPartial) ? 0 : static_cast<int>(gamma_floats * 4);
   } else if (waits) {
     const int sched = (mode == kFusedWait && g_opt_prefetch) ? 1 : 0;
-    if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[sched][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
+    if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[sched][idx[0]][i1]);
     else fn = reinterpret_cast<const void*>(kPublishTable[idx[0]]);
-    name = rows_name(mode, sched, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+    name = rows_name(fmt, mode, sched, idx[0], i1);
   } else if (fast) {
-    const int sched = g_opt_prefetch ? 1 : 0;
-    if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[sched][idx[0]][nseg == 2 ? idx[1] + 1 : 0]);
-    else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[sched][idx[0]]);
-    else fn = reinterpret_cast<const void*>(kPartialTable[sched][idx[0]]);
-    name = rows_name(mode, sched, idx[0], nseg == 2 ? idx[1] + 1 : 0);
+    const int sched = (fmt == kBf16 && g_opt_prefetch) ? 1 : 0;  // pipelining: bf16 kernels only
+    if (fmt == kBf16) {
+      if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable[sched][idx[0]][i1]);
+      else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable[sched][idx[0]]);
+      else fn = reinterpret_cast<const void*>(kPartialTable[sched][idx[0]]);
+    } else {
+      if (mode == kFused) fn = reinterpret_cast<const void*>(kFusedTable8[idx[0]][i1]);
+      else if (mode == kApply) fn = reinterpret_cast<const void*>(kApplyTable8[idx[0]]);
+      else fn = reinterpret_cast<const void*>(kPartialTable8[idx[0]]);
+    }
+    name = rows_name(fmt, mode, sched, idx[0], i1);
   } else {
-    fn = reinterpret_cast<const void*>(kGenericTable[mode]);
-    name = kGenericName[mode];
-    if (mode == kFused && static_cast<int64_t>(max_chunks) * kChunk * 2 <= kMaxStageBytes) {
-      stage_elems = max_chunks * kChunk;
-      lds = stage_elems * 2;
+    fn = reinterpret_cast<const void*>(kGenericTable[fmt][mode]);
+    name = kGenericName[fmt][mode];
+    if (mode == kFused && static_cast<int64_t>(max_chunks) * 16 <= kMaxStageBytes) {
+      stage_elems = max_chunks * fi.per;
+      lds = max_chunks * 16;
     }
   }
+  if (!fn) return QKN_ENOTSUP;  // not reached: every selectable entry is instantiated
   if (g_opt_validate_only) {  // arguments accepted and a kernel chosen; no HIP call
     t_last = qkn_launch_info{name, 0, 0, 0, lds};
     return QKN_OK;
@@ -1131,7 +1273,7 @@ int launch(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps
   int64_t waves_per_cu = static_cast<int64_t>(bpc) * wpb;
   if ((fast || wide) && mode != kFusedWait) {  // a waiting launch keeps every resident slot
     int64_t token_bytes = 0;
-    for (int i = 0; i < nseg; ++i) token_bytes += 2 * static_cast<int64_t>(kp.seg[i].d);
+    for (int i = 0; i < nseg; ++i) token_bytes += fi.esz * static_cast<int64_t>(kp.seg[i].d);
     int64_t want = (kInFlightBytes + token_bytes - 1) / token_bytes;
     if (want < kMinWavesPerCu) want = kMinWavesPerCu;
     if (want < waves_per_cu) waves_per_cu = want;
@@ -1184,16 +1326,17 @@ int validate_common(int64_t T, float eps, int tp, int rank) {
   return QKN_OK;
 }
 
-}  // namespace
+bool seg_dims_bad(const HSeg& s) {
+  return s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
+         s.ldy < s.d_local;
+}
 
-extern "C" {
-
-int qkn_partial_sumsq(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
-                      float* partial_out, void* stream) {
+int partial_impl(const void* x, int64_t ldx, int64_t T, int64_t d_local, float* partial_out,
+                 int fmt, void* stream) {
   if (T < 0 || d_local < 1 || d_local > kMaxWidth || ldx < d_local) return QKN_EINVAL;
   if (T == 0) return QKN_OK;
   if (!x || !partial_out) return QKN_EINVAL;
-  qkn_seg s;
+  HSeg s;
   memset(&s, 0, sizeof(s));
   s.x = x;
   s.ldx = ldx;
@@ -1202,58 +1345,102 @@ int qkn_partial_sumsq(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local
   s.d_full = d_local;
   int rc = check_seg_shape(s, kPartial);
   if (rc != QKN_OK) return rc;
-  rc = check_overlaps(&s, 1, 1, 0, T, kPartial);
+  rc = check_overlaps(&s, 1, 1, 0, T, kPartial, kFormat[fmt].esz);
   if (rc != QKN_OK) return rc;
-  return launch(&s, 1, 1, 0, T, 0.0f, kPartial, stream);
+  return launch(&s, 1, 1, 0, T, 0.0f, kPartial, fmt, stream);
 }
 
-int qkn_apply(const uint16_t* x, int64_t ldx, const float* w, const float* partials, int tp,
-              int64_t T, int64_t d_local, int64_t d_full, float eps, uint16_t* y, int64_t ldy,
-              float* inv_rms, void* stream) {
+int apply_impl(const HSeg& s, int tp, int64_t T, float eps, int fmt, void* stream) {
   int rc = validate_common(T, eps, tp, 0);
   if (rc != QKN_OK) return rc;
-  qkn_seg s;
-  s.x = x;
-  s.ldx = ldx;
-  s.w = w;
-  s.partials = const_cast<float*>(partials);
-  s.y = y;
-  s.ldy = ldy;
-  s.inv_rms = inv_rms;
-  s.d_local = d_local;
-  s.d_full = d_full;
-  if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
-      s.ldy < s.d_local)
-    return QKN_EINVAL;
+  if (seg_dims_bad(s)) return QKN_EINVAL;
   if (T == 0) return QKN_OK;
   rc = check_seg_shape(s, kApply);
   if (rc != QKN_OK) return rc;
-  if (!partials) return QKN_EINVAL;
-  rc = check_overlaps(&s, 1, tp, 0, T, kApply);
+  if (!s.partials) return QKN_EINVAL;
+  rc = check_overlaps(&s, 1, tp, 0, T, kApply, kFormat[fmt].esz);
   if (rc != QKN_OK) return rc;
-  return launch(&s, 1, tp, 0, T, eps, kApply, stream);
+  return launch(&s, 1, tp, 0, T, eps, kApply, fmt, stream);
 }
 
-int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
-                    void* stream) {
-  if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
+int fused_impl(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, int fmt,
+               void* stream) {
   int rc = validate_common(T, eps, tp, rank);
   if (rc != QKN_OK) return rc;
-  for (int i = 0; i < nseg; ++i) {
-    const qkn_seg& s = segs[i];
-    if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
-        s.ldy < s.d_local)
-      return QKN_EINVAL;
-  }
+  for (int i = 0; i < nseg; ++i)
+    if (seg_dims_bad(segs[i])) return QKN_EINVAL;
   if (T == 0) return QKN_OK;
   for (int i = 0; i < nseg; ++i) {
     rc = check_seg_shape(segs[i], kFused);
     if (rc != QKN_OK) return rc;
     if (tp > 1 && !segs[i].partials) return QKN_EINVAL;
   }
-  rc = check_overlaps(segs, nseg, tp, rank, T, kFused);
+  rc = check_overlaps(segs, nseg, tp, rank, T, kFused, kFormat[fmt].esz);
   if (rc != QKN_OK) return rc;
-  return launch(segs, nseg, tp, rank, T, eps, kFused, stream);
+  return launch(segs, nseg, tp, rank, T, eps, kFused, fmt, stream);
+}
+
+template <class S>
+int fused_entry(const S* segs, int nseg, int tp, int rank, int64_t T, float eps, int fmt,
+                void* stream) {
+  if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
+  HSeg h[2];
+  for (int i = 0; i < nseg; ++i) h[i] = to_hseg(segs[i]);
+  return fused_impl(h, nseg, tp, rank, T, eps, fmt, stream);
+}
+
+template <class S>
+int full_entry(const S* segs, int nseg, int64_t T, float eps, int fmt, void* stream) {
+  if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
+  for (int i = 0; i < nseg; ++i)
+    if (segs[i].d_full != segs[i].d_local) return QKN_EINVAL;
+  return fused_entry(segs, nseg, 1, 0, T, eps, fmt, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+int qkn_partial_sumsq(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                      float* partial_out, void* stream) {
+  return partial_impl(x, ldx, T, d_local, partial_out, kBf16, stream);
+}
+
+int qkn_partial_sumsq_fp8(const uint8_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                          float* partial_out, void* stream) {
+  return partial_impl(x, ldx, T, d_local, partial_out, kFp8, stream);
+}
+
+int qkn_apply(const uint16_t* x, int64_t ldx, const float* w, const float* partials, int tp,
+              int64_t T, int64_t d_local, int64_t d_full, float eps, uint16_t* y, int64_t ldy,
+              float* inv_rms, void* stream) {
+  const HSeg s{x, ldx, w, const_cast<float*>(partials), y, ldy, inv_rms, d_local, d_full};
+  return apply_impl(s, tp, T, eps, kBf16, stream);
+}
+
+int qkn_apply_fp8(const uint8_t* x, int64_t ldx, const float* w, const float* partials, int tp,
+                  int64_t T, int64_t d_local, int64_t d_full, float eps, uint8_t* y, int64_t ldy,
+                  float* inv_rms, void* stream) {
+  const HSeg s{x, ldx, w, const_cast<float*>(partials), y, ldy, inv_rms, d_local, d_full};
+  return apply_impl(s, tp, T, eps, kFp8, stream);
+}
+
+int qkn_fused_shard(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
+                    void* stream) {
+  return fused_entry(segs, nseg, tp, rank, T, eps, kBf16, stream);
+}
+
+int qkn_fused_shard_fp8(const qkn_seg8* segs, int nseg, int tp, int rank, int64_t T, float eps,
+                        void* stream) {
+  return fused_entry(segs, nseg, tp, rank, T, eps, kFp8, stream);
+}
+
+int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream) {
+  return full_entry(segs, nseg, T, eps, kBf16, stream);
+}
+
+int qkn_full_fp8(const qkn_seg8* segs, int nseg, int64_t T, float eps, void* stream) {
+  return full_entry(segs, nseg, T, eps, kFp8, stream);
 }
 
 int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
@@ -1262,14 +1449,14 @@ int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_lo
   if (T == 0) return QKN_OK;
   if (!x || !slots_out || epoch == 0 || (reinterpret_cast<uintptr_t>(slots_out) & 7u))
     return QKN_EINVAL;
-  qkn_seg s;
+  HSeg s;
   memset(&s, 0, sizeof(s));
   s.x = x;
   s.ldx = ldx;
   s.d_local = d_local;
   s.d_full = d_local;
   const Span out{reinterpret_cast<uintptr_t>(slots_out), 1, T, T, 8};
-  int rc = check_overlaps(&s, 1, 1, 0, T, kPublish, &out, 1);
+  int rc = check_overlaps(&s, 1, 1, 0, T, kPublish, 2, &out, 1);
   if (rc != QKN_OK) return rc;
   WaitArgs wa;
   memset(&wa, 0, sizeof(wa));
@@ -1278,20 +1465,19 @@ int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_lo
   wa.spin_limit = 1;
   wa.co_resident = 1;
   wa.group = 1;
-  return launch(&s, 1, 1, 0, T, 0.0f, kPublish, stream, &wa);
+  return launch(&s, 1, 1, 0, T, 0.0f, kPublish, kBf16, stream, &wa);
 }
 
-int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
+int qkn_fused_shard_wait(const qkn_seg* segs_in, int nseg, int tp, int rank, int64_t T, float eps,
                          const qkn_wait* wait, void* stream) {
-  if (!segs || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
+  if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
   int rc = validate_common(T, eps, tp, rank);
   if (rc != QKN_OK) return rc;
   if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  HSeg segs[2];
   for (int i = 0; i < nseg; ++i) {
-    const qkn_seg& s = segs[i];
-    if (s.d_local < 1 || s.d_local > kMaxWidth || s.ldx < s.d_local || s.d_full < s.d_local ||
-        s.ldy < s.d_local)
-      return QKN_EINVAL;
+    segs[i] = to_hseg(segs_in[i]);
+    if (seg_dims_bad(segs[i])) return QKN_EINVAL;
   }
   if (T == 0) return QKN_OK;
   if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
@@ -1306,7 +1492,7 @@ int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_
     extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
   }
   extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
-  rc = check_overlaps(segs, nseg, tp, rank, T, kFusedWait, extra, nextra);
+  rc = check_overlaps(segs, nseg, tp, rank, T, kFusedWait, 2, extra, nextra);
   if (rc != QKN_OK) return rc;
   WaitArgs wa;
   wa.slots[0] = wait->slots[0];
@@ -1316,21 +1502,23 @@ int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_
   wa.epoch = wait->epoch;
   wa.co_resident = wait->co_resident;
   wa.group = 1;
-  return launch(segs, nseg, tp, rank, T, eps, kFusedWait, stream, &wa);
+  return launch(segs, nseg, tp, rank, T, eps, kFusedWait, kBf16, stream, &wa);
 }
 
-int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float eps,
+int qkn_fused_group_wait(const qkn_seg* segs_in, int nseg, int tp, int64_t T, float eps,
                          const qkn_wait* wait, void* stream) {
-  if (!segs || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
+  if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
   int rc = validate_common(T, eps, tp, 0);
   if (rc != QKN_OK) return rc;
   if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
-  qkn_seg view[2];  // the full tensors, for shape and overlap checks
+  HSeg segs[2];
+  HSeg view[2];  // the full tensors, for shape and overlap checks
   for (int i = 0; i < nseg; ++i) {
-    const qkn_seg& s = segs[i];
+    const HSeg s = to_hseg(segs_in[i]);
     if (s.d_local < 1 || s.d_local > kMaxWidth || s.d_full != s.d_local * tp ||
         s.ldx < s.d_full || s.ldy < s.d_full)
       return QKN_EINVAL;
+    segs[i] = s;
     view[i] = s;
     view[i].d_local = s.d_full;
     view[i].inv_rms = nullptr;
@@ -1350,7 +1538,7 @@ int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float
       extra[nextra++] = Span{reinterpret_cast<uintptr_t>(segs[i].inv_rms), 1, tp * T, tp * T, 4};
   }
   extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
-  rc = check_overlaps(view, nseg, tp, 0, T, kFusedWait, extra, nextra);
+  rc = check_overlaps(view, nseg, tp, 0, T, kFusedWait, 2, extra, nextra);
   if (rc != QKN_OK) return rc;
   WaitArgs wa;
   wa.slots[0] = wait->slots[0];
@@ -1360,14 +1548,7 @@ int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float
   wa.epoch = wait->epoch;
   wa.co_resident = wait->co_resident;
   wa.group = tp;
-  return launch(segs, nseg, tp, 0, T, eps, kFusedWait, stream, &wa);
-}
-
-int qkn_full(const qkn_seg* segs, int nseg, int64_t T, float eps, void* stream) {
-  if (!segs || nseg < 1 || nseg > 2) return QKN_EINVAL;
-  for (int i = 0; i < nseg; ++i)
-    if (segs[i].d_full != segs[i].d_local) return QKN_EINVAL;
-  return qkn_fused_shard(segs, nseg, 1, 0, T, eps, stream);
+  return launch(segs, nseg, tp, 0, T, eps, kFusedWait, kBf16, stream, &wa);
 }
 
 const char* qkn_strerror(int status) {

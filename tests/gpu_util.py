@@ -18,13 +18,29 @@ def to_dev_bf16(bits: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(DEV)
 
 
+def to_dev_fp8(bits: np.ndarray) -> torch.Tensor:
+    bits = np.ascontiguousarray(bits, dtype=np.uint8)
+    return torch.from_numpy(bits).view(torch.float8_e4m3fn).to(DEV)
+
+
+def to_dev_act(bits: np.ndarray) -> torch.Tensor:
+    """Activation bits to the device: uint8 -> float8_e4m3fn, uint16 -> bfloat16."""
+    return to_dev_fp8(bits) if np.asarray(bits).dtype == np.uint8 else to_dev_bf16(bits)
+
+
 def to_dev_f32(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
 
 
 def bits_of(t: torch.Tensor) -> np.ndarray:
-    """bf16 GPU tensor -> uint16 bits on the host."""
+    """Activation GPU tensor -> bits on the host (uint16 for bf16, uint8 for fp8)."""
+    if t.element_size() == 1:
+        return t.contiguous().view(torch.uint8).cpu().numpy()
     return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def partial_fn(bits: np.ndarray):
+    return L.qkn_partial_sumsq_fp8 if np.asarray(bits).dtype == np.uint8 else L.qkn_partial_sumsq
 
 
 @functools.lru_cache(maxsize=4)
@@ -44,7 +60,8 @@ def peer_partials(data, key, d_full, tp, T, rank, fill_own=np.nan):
     for k in range(tp):
         if k == rank:
             continue
-        L.qkn_partial_sumsq(to_dev_bf16(shard(data, key, d_full, tp, k)), out=P[k])
+        xs = shard(data, key, d_full, tp, k)
+        partial_fn(xs)(to_dev_act(xs), out=P[k])
     return P
 
 
@@ -55,12 +72,12 @@ def run_fused_rank(wl: workloads.Workload, data, rank: int, eps=None):
     segs = []
     for key, gkey, d_full in (("xq", "gq", wl.q_full), ("xk", "gk", wl.k_full)):
         cols = workloads.shard_cols(d_full, tp, rank)
-        segs.append(L.Seg(x=to_dev_bf16(data[key][:, cols]), w=to_dev_f32(data[gkey][cols]),
+        segs.append(L.Seg(x=to_dev_act(data[key][:, cols]), w=to_dev_f32(data[gkey][cols]),
                           d_full=d_full,
                           partials=peer_partials(data, key, d_full, tp, T, rank)
                           if tp > 1 else torch.empty((1, T), dtype=torch.float32, device=DEV),
                           inv_rms=torch.empty(T, dtype=torch.float32, device=DEV)))
-    L.qkn_fused_shard(segs, tp, rank, eps)
+    (L.qkn_fused_shard_fp8 if wl.dtype == "fp8" else L.qkn_fused_shard)(segs, tp, rank, eps)
     info = L.qkn_last_launch()
     torch.cuda.synchronize()
     out = {}

@@ -36,13 +36,15 @@ def dry(lib):
 def _declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(qkn_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(qkn_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_symbols_exported(lib):
     names = _declared_functions()
     assert set(names) >= {"qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
-                          "qkn_strerror", "qkn_last_launch", "qkn_set_option"}
+                          "qkn_strerror", "qkn_last_launch", "qkn_set_option",
+                          "qkn_partial_sumsq_fp8", "qkn_apply_fp8", "qkn_fused_shard_fp8",
+                          "qkn_full_fp8"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -291,6 +293,9 @@ int main(void) {
   printf("qkn_seg %zu\\n", sizeof(qkn_seg)); F(qkn_seg, x); F(qkn_seg, ldx); F(qkn_seg, w);
   F(qkn_seg, partials); F(qkn_seg, y); F(qkn_seg, ldy); F(qkn_seg, inv_rms);
   F(qkn_seg, d_local); F(qkn_seg, d_full);
+  printf("qkn_seg8 %zu\\n", sizeof(qkn_seg8)); F(qkn_seg8, x); F(qkn_seg8, ldx); F(qkn_seg8, w);
+  F(qkn_seg8, partials); F(qkn_seg8, y); F(qkn_seg8, ldy); F(qkn_seg8, inv_rms);
+  F(qkn_seg8, d_local); F(qkn_seg8, d_full);
   printf("qkn_wait %zu\\n", sizeof(qkn_wait)); F(qkn_wait, slots); F(qkn_wait, epoch);
   F(qkn_wait, spin_limit); F(qkn_wait, co_resident); F(qkn_wait, status);
   printf("qkn_launch_info %zu\\n", sizeof(qkn_launch_info)); F(qkn_launch_info, kernel);
@@ -305,7 +310,7 @@ int main(void) {
     c = dict(line.rsplit(" ", 1) for line in
              subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
              if line)
-    for name, cls in (("qkn_seg", L.QknSeg), ("qkn_wait", L.QknWait),
+    for name, cls in (("qkn_seg", L.QknSeg), ("qkn_seg8", L.QknSeg), ("qkn_wait", L.QknWait),
                       ("qkn_launch_info", L.QknLaunchInfo)):
         assert int(c[name]) == ctypes.sizeof(cls), name
         for field, _ in cls._fields_:
@@ -396,3 +401,75 @@ def test_group_entry_validation(dry):
     # the slot array over the full x (T x 4096 bf16 = 512 KiB from BASE)
     assert call([full(1024, 4)], 4, _wait_block(slots=(BASE + 4096, None))) == L.QKN_EOVERLAP
     assert call([full(100, 4)], 4, _wait_block()) == L.QKN_ENOTSUP
+
+
+# ------------------------------------------------------------------ FP8-E4M3
+
+def _fused8(lib, segs, tp, rank, T, eps=1e-6):
+    arr = (L.QknSeg * len(segs))(*segs)  # qkn_seg8 has qkn_seg's layout
+    return lib.qkn_fused_shard_fp8(arr, len(segs), tp, rank, T, ctypes.c_float(eps), None)
+
+
+@pytest.mark.parametrize("d,expect", [(16, "rows_fp8<1,0>"), (1024, "rows_fp8<1,0>"),
+                                      (1040, "rows_fp8<2,0>"), (2048, "rows_fp8<2,0>"),
+                                      (4096, "rows_fp8<4,0>"), (4112, "wide_fp8<8,0>"),
+                                      (8192, "wide_fp8<8,0>"), (8208, "wide_fp8<16,0>"),
+                                      (16384, "wide_fp8<16,0>"), (16400, "generic_fp8"),
+                                      (8, "generic_fp8"), (1000, "generic_fp8")])
+def test_fp8_path_choice_by_width(dry, d, expect):
+    seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
+    assert _fused8(dry, [seg], 2, 0, 16) == 0
+    name = L.qkn_last_launch()["kernel"]
+    assert name.startswith(expect + ("/" if expect.startswith("generic") else "")), name
+
+
+def test_fp8_entry_points_validate_like_bf16(dry):
+    q = _seg(BASE, 2048, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 2048, 2048, 4096)
+    k = _seg(BASE + 256 * MB, 512, BASE + 300 * MB, BASE + 301 * MB, BASE + 400 * MB, 512, 512, 1024)
+    assert _fused8(dry, [q, k], 2, 1, 8192) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,1>/fused"
+    assert dry.qkn_partial_sumsq_fp8(BASE, 2048, 64, 2048, BASE + 64 * MB, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,0>/partial"
+    assert dry.qkn_apply_fp8(BASE, 2048, BASE + 64 * MB, BASE + 65 * MB, 2, 64, 2048, 4096,
+                             ctypes.c_float(1e-6), BASE + 128 * MB, 2048, None, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,0>/apply"
+    full = (L.QknSeg * 2)(_seg(BASE, 4096, BASE + 64 * MB, 0, BASE + 128 * MB, 4096, 4096, 4096),
+                          _seg(BASE + 256 * MB, 1024, BASE + 300 * MB, 0, BASE + 400 * MB, 1024,
+                               1024, 1024))
+    assert dry.qkn_full_fp8(full, 2, 8192, ctypes.c_float(1e-6), None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_fp8<4,1>/fused"
+    # the prefetch option is a bf16-only variant; fp8 ignores it
+    assert dry.qkn_set_option(b"prefetch", 1) == 0
+    assert _fused8(dry, [q, k], 2, 1, 8192) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,1>/fused"
+    # invalid arguments as for bf16
+    assert _fused8(dry, [q, k], 2, 2, 64) == L.QKN_EINVAL
+    assert _fused8(dry, [_seg(BASE, 2048, BASE + 64 * MB, 0, BASE + 128 * MB, 2048, 2048, 4096)],
+                   2, 0, 64) == L.QKN_EINVAL  # partials NULL with tp > 1
+    assert dry.qkn_full_fp8(full, 3, 8, ctypes.c_float(1e-6), None) == L.QKN_EINVAL
+    assert dry.qkn_partial_sumsq_fp8(None, 8, 4, 8, BASE, None) == L.QKN_EINVAL
+    assert dry.qkn_apply_fp8(BASE, 8, BASE + MB, None, 1, 4, 8, 8, ctypes.c_float(0.0),
+                             BASE + 2 * MB, 8, None, None) == L.QKN_EINVAL
+
+
+def test_fp8_alignment_and_overlap_in_bytes(dry):
+    # a stride of 8 elements is 16-byte aligned for bf16 but not a whole fp8 chunk
+    seg = _seg(BASE, 1032, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1032, 1024, 2048)
+    assert _fused8(dry, [seg], 2, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic_fp8/fused"
+    seg = _seg(BASE + 8, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 2048)
+    assert _fused8(dry, [seg], 2, 0, 16) == 0
+    assert L.qkn_last_launch()["kernel"] == "generic_fp8/fused"
+    # y directly after x (T rows of 1024 bytes) does not overlap; one byte earlier does
+    T = 64
+    x, y = BASE, BASE + T * 1024
+    seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, y, 1024, 1024, 2048)
+    assert _fused8(dry, [seg], 2, 0, T) == 0
+    seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, y - 1, 1024, 1024, 2048)
+    assert _fused8(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
+    # the bf16 entry sees the same y overlapping (2-byte elements)
+    seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, y, 1024, 1024, 2048)
+    assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
+    # in place is allowed
+    seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, x, 1024, 1024, 2048)
+    assert _fused8(dry, [seg], 2, 0, T) == 0

@@ -8,6 +8,10 @@
   of sqrt(ms / (ms + eps)); power-of-two scaling with eps = 0 leaves the output
   unchanged bit for bit; concatenating the TP shards gives the unsharded
   output for every TP degree; Q and K are normalised independently;
+* FP8-E4M3: hand-worked codes, encodings and a QK-Norm case (tests/golden),
+  every one of the 256 codes against torch's float8_e4m3fn, the encoder
+  against torch's cast on a dense fp32 sweep holding every halfway case, and
+  the FP8 path against torch's RMSNorm on decoded inputs;
 * mutation tests: plausible mistakes planted in the oracle must each fail at
   least one of the pins above.
 """
@@ -27,6 +31,7 @@ from oracle import compare
 from oracle import qknorm as Q
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_checks.json")
+GOLDEN_FP8 = os.path.join(os.path.dirname(__file__), "golden", "fp8_hand_checks.json")
 
 
 def _golden_cases():
@@ -85,6 +90,93 @@ def check_bf16_decode_exhaustive():
     assert np.array_equal(ours[~nan], ref[~nan])
     # signed zeros keep their sign
     assert np.array_equal(np.signbit(ours[~nan]), np.signbit(ref[~nan]))
+
+
+def _fp8_golden():
+    with open(GOLDEN_FP8) as f:
+        return json.load(f)
+
+
+def _codes(rows):
+    return np.array([[int(v, 16) for v in r] for r in rows], dtype=np.uint8)
+
+
+def check_fp8_golden():
+    g = _fp8_golden()
+    for c in g["decode"]:
+        v = Q.decode_e4m3(np.array([int(c["code"], 16)], np.uint8))[0]
+        want = _num(c["value"])
+        if math.isnan(want):
+            assert math.isnan(v), c
+        else:
+            assert v == want and math.copysign(1, v) == math.copysign(1, want), c
+    for c in g["encode"]:
+        got = int(Q.encode_e4m3(np.array([c["value"]], np.float64))[0])
+        assert got == int(c["code"], 16), (c, hex(got))
+    for case in g["cases"]:
+        x = _codes(case["x_codes"])
+        tp, eps = case["tp"], case["eps"]
+        d_local = x.shape[1] // tp
+        y_full = _as_array(case["y_full"])
+        for r in range(tp):
+            out = Q.qknorm_shard(x, np.array(case["gamma"], np.float32), tp, r, eps, fmt="fp8")
+            assert np.array_equal(out["partials"], np.array(case["partials"], np.float64))
+            compare.check_close(out["inv"], np.array(case["inv"]), 1e-15, case["name"])
+            ys = y_full[:, r * d_local:(r + 1) * d_local]
+            compare.check_close(out["y"], ys, 1e-15, case["name"])
+            codes = _codes(case["y_codes"])[:, r * d_local:(r + 1) * d_local]
+            assert np.array_equal(Q.encode_e4m3(out["y"]), codes), case["name"]
+
+
+def _torch_e4m3(codes):
+    return torch.from_numpy(np.asarray(codes, np.uint8)).view(torch.float8_e4m3fn).double().numpy()
+
+
+def check_e4m3_decode_exhaustive():
+    codes = np.arange(256, dtype=np.uint8)
+    ours, ref = Q.decode_e4m3(codes), _torch_e4m3(codes)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan) and nan.sum() == 2
+    assert np.array_equal(ours[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(ours[~nan]), np.signbit(ref[~nan]))
+
+
+def _fp32_sweep():
+    """fp32 values: every finite code value, every halfway point between
+    neighbours and the fp32 numbers on either side of it, the overflow edge,
+    and scaled normal draws."""
+    vals = np.unique(_torch_e4m3(np.arange(256, dtype=np.uint8)))
+    vals = vals[np.isfinite(vals)]
+    mids = ((vals[1:] + vals[:-1]) / 2).astype(np.float32)
+    edge = np.array([448, 456, 464, 472, 480, 1e6, np.inf], np.float32)
+    mids = np.concatenate([mids, edge, -edge])
+    rng = np.random.default_rng(7)
+    draws = (rng.standard_normal(50000) * rng.choice([1e-3, 0.1, 1, 30, 400], 50000)).astype(np.float32)
+    return np.concatenate([vals.astype(np.float32), mids, np.nextafter(mids, np.float32(np.inf)),
+                           np.nextafter(mids, np.float32(-np.inf)), draws,
+                           np.array([0.0, -0.0, np.nan], np.float32)])
+
+
+def check_e4m3_encode_against_torch():
+    x = _fp32_sweep()
+    ours = Q.encode_e4m3(x.astype(np.float64))
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    bad = np.nonzero(ours != ref)[0]
+    assert bad.size == 0, [(float(x[i]), hex(ours[i]), hex(ref[i])) for i in bad[:5]]
+    codes = np.arange(256, dtype=np.uint8)
+    finite = ~np.isnan(Q.decode_e4m3(codes))
+    assert np.array_equal(Q.encode_e4m3(Q.decode_e4m3(codes[finite])), codes[finite])
+
+
+def check_fp8_library_rmsnorm():
+    for T, d, eps, scale, tp in [(16, 512, 1e-6, 1.0, 2), (5, 96, 1e-3, 20.0, 3),
+                                 (3, 64, 0.0, 0.01, 4)]:
+        codes = workloads.random_rows(d, T, d, "student_t", scale, dtype="fp8")
+        g = workloads.random_gamma(d, d)
+        x = torch.from_numpy(_torch_e4m3(codes))
+        ref = torch.nn.functional.rms_norm(x, (d,), torch.from_numpy(g.astype(np.float64)), eps).numpy()
+        parts = [Q.qknorm_shard(codes, g, tp, r, eps, fmt="fp8")["y"] for r in range(tp)]
+        compare.check_close(np.concatenate(parts, axis=1), ref, 1e-12, f"fp8 rms_norm d={d}")
 
 
 def check_library_rmsnorm(seed=0):
@@ -167,7 +259,9 @@ def check_layerwise_independent():
 
 ALL_PINS = [check_golden, check_bf16_decode_exhaustive, check_library_rmsnorm,
             check_fsum_partials, check_concat_equals_unsharded, check_gamma_one_closed_form,
-            check_scale_invariance, check_layerwise_independent]
+            check_scale_invariance, check_layerwise_independent, check_fp8_golden,
+            check_e4m3_decode_exhaustive, check_e4m3_encode_against_torch,
+            check_fp8_library_rmsnorm]
 
 
 @pytest.mark.parametrize("pin", ALL_PINS, ids=lambda f: f.__name__)
@@ -192,6 +286,19 @@ def test_nan_and_inf_propagate():
     assert out["partials"][1, 0] == 13.0
     assert out["inv"][1] == 0.0 and out["y"][1, 0] == 0.0  # inf sum -> factor 0
     assert np.isfinite(out["y"][2]).all()
+
+
+def test_compare_fp8_rule():
+    ref = np.array([1.03, 1.0625, 1.0625 * (1 + 1e-7), 0.0, 470.0, 464.0, np.nan, 1.5e-3, -2.6])
+    ok = np.array([1.0, 1.0, 1.125, 0.0, np.nan, 448.0, np.nan, 2 ** -9, -2.5])
+    assert compare.check_fp8(ok, ref, "ok") <= 1.0 + 1e-3
+    for i, bad in [(0, 1.125), (3, 2 ** -9), (4, 448.0), (5, 416.0), (6, 1.0), (7, 0.0), (8, -2.75)]:
+        t = ok.copy()
+        t[i] = bad
+        with pytest.raises(AssertionError):
+            compare.check_fp8(t, ref, f"bad {i}")
+    assert np.array_equal(compare.e4m3_half_step(np.array([0.0, 2 ** -8, 1.0, 1.99, 300.0])),
+                          np.array([2 ** -10, 2 ** -10, 2 ** -4, 2 ** -4, 16.0]))
 
 
 def test_compare_rules():
@@ -256,9 +363,9 @@ def _mut_decode_truncated(bits):
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def _mut_local_stat(x_bits, gamma, tp, rank, eps, row_block=1024):
+def _mut_local_stat(x_bits, gamma, tp, rank, eps, row_block=1024, fmt="bf16"):
     # the classic TP mistake: normalise the shard with its own statistic
-    x = Q.decode_bf16(x_bits)
+    x = Q.decode(x_bits, fmt)
     cols = Q.shard_slice(x.shape[1], tp, rank)
     P = Q.shard_partials(x, tp)
     xs = x[:, cols]
@@ -267,9 +374,9 @@ def _mut_local_stat(x_bits, gamma, tp, rank, eps, row_block=1024):
             "y": xs * inv[:, None] * np.asarray(gamma, np.float64)[cols][None, :]}
 
 
-def _mut_joint_qk(xq_bits, xk_bits, gq, gk, tp, rank, eps, row_block=1024):
+def _mut_joint_qk(xq_bits, xk_bits, gq, gk, tp, rank, eps, row_block=1024, fmt="bf16"):
     # one factor over Q and K together instead of one per tensor
-    xq, xk = Q.decode_bf16(xq_bits), Q.decode_bf16(xk_bits)
+    xq, xk = Q.decode(xq_bits, fmt), Q.decode(xk_bits, fmt)
     S = Q.sum_of_squares(xq) + Q.sum_of_squares(xk)
     inv = Q.rms_factor(S, xq.shape[1] + xk.shape[1], eps)
     out = {}
@@ -287,6 +394,48 @@ def _mut_partials_reversed(x_full, tp):
                      for k in reversed(range(tp))])
 
 
+def _mut_e4m3_bias8(bits):
+    b = np.asarray(bits, np.uint8).astype(np.int64)
+    E, M = (b >> 3) & 0xF, b & 7
+    mag = np.where(E == 0, M * 2.0 ** -10, (8 + M) * np.exp2(E - 11.0))
+    out = np.where(b >> 7, -mag, mag)
+    out[(E == 15) & (M == 7)] = np.nan
+    return out
+
+
+def _mut_e4m3_no_subnormals(bits):
+    b = np.asarray(bits, np.uint8).astype(np.int64)
+    E, M = (b >> 3) & 0xF, b & 7
+    mag = (8 + M) * np.exp2(E - 10.0)  # E = 0 read as a normal binade
+    out = np.where(b >> 7, -mag, mag)
+    out[(E == 15) & (M == 7)] = np.nan
+    return out
+
+
+def _mut_e4m3_inf_code(bits):
+    out = Q_ORIG["decode_e4m3"](bits)
+    b = np.asarray(bits, np.uint8)
+    out[(b & 0x7F) == 0x7F] = np.where(b[(b & 0x7F) == 0x7F] >> 7, -np.inf, np.inf)
+    return out
+
+
+def _mut_encode_ties_away(v):
+    v = np.asarray(v, np.float64)
+    step = np.exp2(np.maximum(np.frexp(np.where(v != 0, np.abs(v), 1.0))[1] - 1, -6) - 3.0)
+    nudged = np.abs(v) + step * 1e-9  # halfway cases now round up in magnitude
+    return Q_ORIG["encode_e4m3"](np.copysign(nudged, v))
+
+
+def _mut_encode_saturates(v):
+    return Q_ORIG["encode_e4m3"](np.clip(np.asarray(v, np.float64), -448.0, 448.0))
+
+
+def _mut_decode_ignores_format(bits, fmt="bf16"):
+    return Q_ORIG["decode_bf16"](np.asarray(bits).astype(np.uint16))
+
+
+Q_ORIG = {name: getattr(Q, name) for name in ("decode_e4m3", "encode_e4m3", "decode_bf16")}
+
 MUTANTS = {
     "eps_outside_sqrt": ("rms_factor", _mut_eps_outside),
     "divisor_off_by_one": ("rms_factor", _mut_divisor_off_by_one),
@@ -301,6 +450,12 @@ MUTANTS = {
     "local_statistic": ("qknorm_shard", _mut_local_stat),
     "joint_qk_factor": ("qknorm_layerwise", _mut_joint_qk),
     "partials_rank_reversed": ("shard_partials", _mut_partials_reversed),
+    "e4m3_bias_8": ("decode_e4m3", _mut_e4m3_bias8),
+    "e4m3_no_subnormals": ("decode_e4m3", _mut_e4m3_no_subnormals),
+    "e4m3_has_infinity": ("decode_e4m3", _mut_e4m3_inf_code),
+    "e4m3_ties_away": ("encode_e4m3", _mut_encode_ties_away),
+    "e4m3_saturating_encode": ("encode_e4m3", _mut_encode_saturates),
+    "fp8_read_as_bf16": ("decode", _mut_decode_ignores_format),
 }
 
 

@@ -1,7 +1,7 @@
 """Seeded synthetic workloads for sharded layerwise QK-Norm.
 
-This module only draws inputs: projected Q and K activations (as bf16 bit
-patterns), the fp32 gamma vectors, and the shard layout. It holds none of the
+This module only draws inputs: projected Q and K activations (as bf16 or
+FP8-E4M3 bit patterns), the fp32 gamma vectors, and the shard layout. It holds none of the
 normalisation arithmetic, so both the fp64 oracle and the HIP path can take
 their inputs from here without sharing any of the method's code.
 
@@ -20,8 +20,10 @@ Recipe (shared by every workload):
     from ``SeedSequence([seed, stream_id, b])``, so blocks can be drawn in
     parallel and the bits do not depend on the number of threads;
   * activations are drawn in fp32, shaped by the workload's distribution,
-    then rounded to bf16 with round-to-nearest-even; everyone consumes the
-    same bf16 bits;
+    then rounded to the workload's format with round-to-nearest-even: bf16,
+    or FP8-E4M3 (OCP e4m3fn) after clamping to its finite range [-448, 448]
+    (a saturating quantiser, as FP8 activations are produced in practice);
+    everyone consumes the same bits;
   * lognormal(mu, sigma) = exp(N(mu, sigma)), one draw per token per tensor,
     multiplying that token's whole (unsharded) row;
   * outlier channels: n = max(1, round(0.001 * d_full)) channels per tensor,
@@ -58,6 +60,7 @@ class Workload:
     sigma: float = 0.0  # lognormal sigma for "normal_lognormal"
     df: float = 3.0  # degrees of freedom for "student_t"
     eps: float = 1e-6
+    dtype: str = "bf16"  # activation format: "bf16" | "fp8" (FP8-E4M3)
 
     @property
     def q_local(self) -> int:
@@ -75,6 +78,12 @@ class Workload:
 
     def with_tokens(self, T: int) -> "Workload":
         return replace(self, T=T, name=f"{self.name}@T{T}")
+
+    def with_dtype(self, dtype: str) -> "Workload":
+        """Same draws, quantised to another activation format."""
+        if dtype not in ("bf16", "fp8"):
+            raise ValueError(dtype)
+        return replace(self, dtype=dtype, name=f"{self.name}@{dtype}")
 
 
 # The five workloads. Seeds: the tiny case uses seed 0; the others 1..4.
@@ -107,6 +116,35 @@ def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     return rounded
 
 
+E4M3_MAX = 448.0
+
+
+def f32_to_e4m3_bits(a: np.ndarray) -> np.ndarray:
+    """Quantise fp32 values to FP8-E4M3 (OCP e4m3fn) bits, saturating.
+
+    Input conversion only (the data format), not part of the normalisation.
+    Values are clamped to [-448, 448], then rounded to the nearest code (ties
+    to the even code); magnitudes below 2^-6 use the subnormal grid 2^-9.
+    NaN maps to 0x7f (0xff if negative).
+    """
+    a = np.asarray(a, dtype=np.float32).astype(np.float64)
+    nan = np.isnan(a)
+    neg = np.signbit(a)
+    m = np.minimum(np.abs(np.where(nan, 0.0, a)), E4M3_MAX)
+    # binade exponent of m (m = f * 2^k, 0.5 <= f < 1), at least -6
+    k = np.frexp(np.where(m > 0, m, 1.0))[1] - 1
+    k = np.where(m > 0, np.maximum(k, -6), -6)
+    units = np.round(m * np.exp2(3.0 - k))  # multiples of the grid step 2^(k-3); half to even
+    # units is in [0, 16]; 16 means the next binade's 1.000
+    normal = (k > -6) | (units >= 8)
+    exp_field = np.where(normal, k + 7 + (units >= 16), 0)
+    mant = np.where(units >= 16, 0, np.where(normal, units - 8, units))
+    bits = (exp_field.astype(np.int64) << 3) | mant.astype(np.int64)
+    bits = bits | (neg.astype(np.int64) << 7)
+    bits = np.where(nan, np.where(neg, 0xFF, 0x7F), bits)
+    return bits.astype(np.uint8)
+
+
 def _rng(seed: int, stream: int) -> np.random.Generator:
     return np.random.default_rng(np.random.SeedSequence([seed, stream]))
 
@@ -120,7 +158,7 @@ def _threads() -> int:
 
 
 def _activations(wl: Workload, d_full: int, stream: int, scale_col: int) -> np.ndarray:
-    """bf16 bits [T, d_full] of one tensor, drawn block by block."""
+    """Activation bits [T, d_full] of one tensor, drawn block by block."""
     if wl.dist not in ("normal", "student_t", "normal_lognormal", "normal_outliers"):
         raise ValueError(f"unknown distribution {wl.dist!r}")
     T = wl.T
@@ -130,7 +168,10 @@ def _activations(wl: Workload, d_full: int, stream: int, scale_col: int) -> np.n
         s = np.exp(_rng(wl.seed, STREAM_SCALE).normal(0.0, wl.sigma, size=(T, 2)))
         scale = s[:, scale_col:scale_col + 1].astype(np.float32)
     idx = outlier_channels(wl)[scale_col] if wl.dist == "normal_outliers" else None
-    out = np.empty((T, d_full), dtype=np.uint16)
+    fp8 = wl.dtype == "fp8"
+    if wl.dtype not in ("bf16", "fp8"):
+        raise ValueError(f"unknown activation format {wl.dtype!r}")
+    out = np.empty((T, d_full), dtype=np.uint8 if fp8 else np.uint16)
 
     def block(b: int) -> None:
         t0, t1 = b * BLOCK_TOKENS, min(T, (b + 1) * BLOCK_TOKENS)
@@ -143,7 +184,7 @@ def _activations(wl: Workload, d_full: int, stream: int, scale_col: int) -> np.n
             x *= scale[t0:t1]
         if idx is not None:
             x[:, idx] *= np.float32(50.0)
-        out[t0:t1] = f32_to_bf16_bits(x)
+        out[t0:t1] = f32_to_e4m3_bits(x) if fp8 else f32_to_bf16_bits(x)
 
     nblocks = (T + BLOCK_TOKENS - 1) // BLOCK_TOKENS
     if nblocks <= 1:
@@ -170,8 +211,9 @@ def outlier_channels(wl: Workload) -> Tuple[np.ndarray, np.ndarray]:
 def generate(wl: Workload) -> Dict[str, np.ndarray]:
     """Full (unsharded) inputs of a workload.
 
-    Returns ``xq`` uint16 [T, q_full], ``xk`` uint16 [T, k_full] (bf16 bits),
-    ``gq`` float32 [q_full], ``gk`` float32 [k_full].
+    Returns ``xq`` [T, q_full], ``xk`` [T, k_full] (bf16 bits as uint16, or
+    FP8-E4M3 bits as uint8 when ``wl.dtype == "fp8"``), ``gq`` float32
+    [q_full], ``gk`` float32 [k_full].
     """
     xq = _activations(wl, wl.q_full, STREAM_XQ, 0)
     xk = _activations(wl, wl.k_full, STREAM_XK, 1)
@@ -188,8 +230,9 @@ def shard_cols(d_full: int, tp: int, rank: int) -> slice:
     return slice(rank * d_local, (rank + 1) * d_local)
 
 
-def random_rows(seed: int, T: int, d: int, dist: str = "normal", scale: float = 1.0) -> np.ndarray:
-    """Small ad-hoc bf16 inputs for edge-case tests (uint16 bits, [T, d])."""
+def random_rows(seed: int, T: int, d: int, dist: str = "normal", scale: float = 1.0,
+                dtype: str = "bf16") -> np.ndarray:
+    """Small ad-hoc inputs for edge-case tests ([T, d] bits: uint16 bf16 or uint8 FP8)."""
     rng = _rng(seed, 100)
     if dist == "normal":
         x = rng.standard_normal(size=(T, d), dtype=np.float32)
@@ -199,7 +242,8 @@ def random_rows(seed: int, T: int, d: int, dist: str = "normal", scale: float = 
         x = rng.uniform(-1.0, 1.0, size=(T, d)).astype(np.float32)
     else:
         raise ValueError(dist)
-    return f32_to_bf16_bits(x * np.float32(scale))
+    x = x * np.float32(scale)
+    return f32_to_e4m3_bits(x) if dtype == "fp8" else f32_to_bf16_bits(x)
 
 
 def random_gamma(seed: int, d: int) -> np.ndarray:
