@@ -48,7 +48,7 @@ def parse():
                    help="only the headline workload (for profiler runs)")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--summarize", metavar="DIR",
-                   help="print summaries of rocprofv3 CSV output in DIR and exit")
+                   help="write the profiles/ summaries from rocprofv3 CSV output in DIR and exit")
     p.add_argument("--calibration-copy", action="store_true",
                    help="also run a plain device copy of Q's input (known bytes) a few times, "
                         "to scale profiler byte counters")
@@ -268,14 +268,39 @@ def traffic_bytes(kernel: str, workload: str):
         return None
 
 
-def summarize(outdir: str, workload: str) -> None:
-    """Write profile summaries from rocprofv3 CSV output in `outdir`:
-    trace/*_kernel_trace.csv (kernel trace of the default bench run) and
-    pmc_fetch/*_counter_collection.csv, pmc_write/*_counter_collection.csv
-    (FETCH_SIZE / WRITE_SIZE runs with --no-extras --calibration-copy)."""
+def trace_name(launch_name: str) -> str:
+    """Profiler (demangled) name of the kernel a launch name denotes, e.g.
+    "rows<4,1>/fused" -> "void qkn_rows<FmtBf16, 4, 1, 0, 0>"."""
+    import re
+    m = re.fullmatch(r"(rows|rows_pf|rows_fp8|wide|wide_fp8)<(\d+),(\d+)>/(\w+)", launch_name)
+    if not m:
+        raise ValueError(f"no profiler name for {launch_name!r}")
+    fam, n0, n1, mode = m.groups()
+    fmt = "FmtFp8" if fam.endswith("fp8") else "FmtBf16"
+    mode_id = ["fused", "apply", "partial", "fused_wait", "publish"].index(mode)
+    if fam.startswith("wide"):
+        return f"void qkn_wide<{fmt}, {n0}, {n1}, {mode_id}>"
+    return f"void qkn_rows<{fmt}, {n0}, {n1}, {mode_id}, {1 if fam == 'rows_pf' else 0}>"
+
+
+def summarize(outdir: str) -> None:
+    """Write the profile summaries of the headline kernel into profiles/ from
+    rocprofv3 CSV output in `outdir`:
+      trace/*_kernel_trace.csv and trace_bench.json -- kernel trace of the
+        default bench run and that run's JSON line;
+      pmc_fetch/, pmc_write/ -- FETCH_SIZE and WRITE_SIZE runs of
+        ``bench.py --no-extras --calibration-copy``.
+    Counters are scaled by what they read for the calibration copy (a plain
+    device copy of Q's input, known bytes)."""
     import csv
     import glob
     import statistics
+    bench = json.loads(open(os.path.join(outdir, "trace_bench.json")).read().strip().splitlines()[-1])
+    kernel, workload = bench["config"]["kernel"], bench["config"]["workload"]
+    algo = bench["roofline"]["algorithmic_bytes"]
+    tname = trace_name(kernel)
+    grid_threads = bench["config"]["grid"] * bench["config"]["block"]
+
     trace = glob.glob(os.path.join(outdir, "trace", "*_kernel_trace.csv"))[0]
     rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
     runs = []  # consecutive dispatches of one kernel and launch shape
@@ -294,13 +319,41 @@ def summarize(outdir: str, workload: str) -> None:
         sd = sorted(ds)
         return (f"| {name} | {g} | {w} | {len(ds)} | {statistics.mean(ds) / 1e3:.3f} | "
                 f"{sd[len(sd) // 2] / 1e3:.3f} | {sd[0] / 1e3:.3f} | {sd[-1] / 1e3:.3f} |")
-    print("Runs of at least 5 consecutive dispatches of one kernel and shape, in order:\n")
-    print("\n".join(head + [row(*k, ds) for k, ds in runs if len(ds) >= 5]))
+    headline = next(ds for (n, g, _), ds in runs if n == tname and g == grid_threads and len(ds) >= 20)
+    mean_us = statistics.mean(headline) / 1e3
     total = {}
     for k, ds in runs:
         total.setdefault(k, []).extend(ds)
-    print("\nAll dispatches per kernel and shape:\n")
-    print("\n".join(head + [row(*k, ds) for k, ds in sorted(total.items(), key=lambda kv: -sum(kv[1]))]))
+    sha = source_sha256()
+    tag = os.path.basename(counters_path(kernel, workload))[len("counters_"):-len(".txt")]
+    plain = []  # the untraced bench.py run of the same session, if there is one
+    if os.path.exists(os.path.join(outdir, "bench.json")):
+        pb = json.loads(open(os.path.join(outdir, "bench.json")).read().strip().splitlines()[-1])
+        if pb["config"]["kernel"] == kernel:
+            k_us = pb["roofline"]["kernel_us"]
+            plain = [f"The untraced `python bench.py` run of the same session: kernel_us {k_us} "
+                     f"(timed region / launches), {abs(k_us - mean_us) / mean_us:.1%} from the "
+                     f"trace's mean; value {pb['value']} GB/s, roofline.frac {pb['roofline']['frac']}."]
+    cmd_trace = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/trace -o bench "
+                 "-- python -u bench.py --no-cpu-baseline > gpurun_out/trace_bench.json")
+    lines = [f"# Kernel trace: {kernel} on {workload}", "",
+             f"Kernel source sha256 {sha}. Commands (MI355X, repository root):", "",
+             f"    {cmd_trace}", "    python bench.py --summarize gpurun_out", "",
+             f"Headline kernel `{tname}` (launch name `{kernel}`), the run of {len(headline)} "
+             f"consecutive dispatches of the bench's timed and per-launch passes: mean "
+             f"{mean_us:.3f} us -> {algo} algorithmic bytes / {mean_us:.3f} us = "
+             f"{algo / (mean_us * 1e-6) / 1e9:.0f} GB/s = {algo / (mean_us * 1e-6) / 1e9 / HBM_PEAK_GBS:.1%} "
+             f"of 8 TB/s. The traced bench.py line (tracing adds gaps between launches): kernel_us "
+             f"{bench['roofline']['kernel_us']} (timed region / launches)."] + plain + [
+             "", "Kernel names: `qkn_rows<Fmt, N0, N1, MODE, SCHED>` / `qkn_wide<Fmt, N0, N1, MODE>`, "
+             "N0/N1 = 16-byte chunks per lane of the two tensors, MODE 0 fused, 1 apply (Phases B+C), "
+             "2 Phase A, 3 fused with wait, 4 publish; SCHED 1 = pipelined.", "",
+             "Runs of at least 20 consecutive dispatches of one kernel and shape, in order:", ""]
+    lines += head + [row(*k, ds) for k, ds in runs if len(ds) >= 20]
+    lines += ["", "All dispatches per kernel and shape:", ""]
+    lines += head + [row(*k, ds) for k, ds in sorted(total.items(), key=lambda kv: -sum(kv[1]))]
+    with open(os.path.join(ROOT, "profiles", f"trace_{tag}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
     def counter(sub):
         f = glob.glob(os.path.join(outdir, sub, "*_counter_collection.csv"))[0]
@@ -310,15 +363,32 @@ def summarize(outdir: str, workload: str) -> None:
             by.setdefault(name, []).append(float(r["Counter_Value"]))
         return by
     fetch, write = counter("pmc_fetch"), counter("pmc_write")
-    # calibration: the largest plain device copy (Q's input, known bytes)
-    cal_f = max(fetch["__amd_rocclr_copyBuffer"])
-    cal_w = max(write["__amd_rocclr_copyBuffer"])
-    print(f"\ncalibration copy: FETCH_SIZE {cal_f:.1f} KiB, WRITE_SIZE {cal_w:.1f} KiB")
-    for name in fetch:
-        if not name.startswith("void qkn_rows"):
-            continue
-        print(f"{name}: FETCH_SIZE {statistics.mean(fetch[name]):.1f} KiB, "
-              f"WRITE_SIZE {statistics.mean(write[name]):.1f} KiB per dispatch")
+    cal_f, cal_w = max(fetch["__amd_rocclr_copyBuffer"]), max(write["__amd_rocclr_copyBuffer"])
+    cal_bytes = bench["config"]["tokens"] * bench["config"]["q_local"] * (1 if "fp8" in kernel else 2)
+    sf, sw = cal_bytes / 1024 / cal_f, cal_bytes / 1024 / cal_w
+    kf, kw = statistics.mean(fetch[tname]), statistics.mean(write[tname])
+    hbm = int(round(kf * 1024 * sf + kw * 1024 * sw))
+    out = [f"kernel: {kernel} ({tname})", f"workload: {workload}", f"source_sha256: {sha}",
+           "commands (on the MI355X, from the repository root):",
+           "  rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o f -- python -u "
+           "bench.py --steps 20 --warmup 2 --no-cpu-baseline --no-extras --calibration-copy",
+           "  rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o w -- python -u "
+           "bench.py --steps 20 --warmup 2 --no-cpu-baseline --no-extras --calibration-copy",
+           "  python bench.py --summarize gpurun_out",
+           f"calibration copy (device copy of Q's input, {cal_bytes // 1024} KiB read and written):",
+           f"  FETCH_SIZE {cal_f:.1f} KiB -> scale {sf:.4f}",
+           f"  WRITE_SIZE {cal_w:.1f} KiB -> scale {sw:.4f}",
+           f"fused kernel, mean over {len(fetch[tname])} dispatches:",
+           f"  FETCH_SIZE {kf:.1f} KiB -> {int(round(kf * 1024 * sf))} bytes after scaling",
+           f"  WRITE_SIZE {kw:.1f} KiB -> {int(round(kw * 1024 * sw))} bytes after scaling",
+           f"algorithmic_bytes_per_launch: {algo}",
+           f"hbm_bytes_per_launch: {hbm}",
+           f"traffic_over_algorithmic: {hbm / algo:.4f}"]
+    with open(counters_path(kernel, workload), "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+    print(f"trace: headline mean {mean_us:.3f} us over {len(headline)} dispatches; "
+          f"bench kernel_us {bench['roofline']['kernel_us']}")
 
 
 def cpu_baseline(wl, rank, data, seconds):
@@ -350,7 +420,7 @@ def cpu_baseline(wl, rank, data, seconds):
 def main():
     args = parse()
     if args.summarize:
-        summarize(args.summarize, args.workload)
+        summarize(args.summarize)
         return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -267,10 +267,10 @@ int qkn_last_launch(qkn_launch_info* info);
  * Process-wide tuning knobs (for benchmarks and tests; not thread-safe with
  * concurrent launches). Keys:
  *   "waves_per_cu"   wavefronts per CU used to size the grid (0 = the
- *                    default: enough to keep ~24 KB of rows requested per
- *                    CU, at least 6, at most the occupancy limit; larger
- *                    values oversubscribe, which is correct but not
- *                    persistent);
+ *                    default: enough to keep ~24 KB (bf16) or ~32 KB (fp8)
+ *                    of rows requested per CU, at least 6, at most the
+ *                    occupancy limit; larger values oversubscribe, which is
+ *                    correct but not persistent);
  *   "prefetch"       1 = pipelined kernels that request the next token
  *                    before writing the current one (bf16 register path),
  *                    0 = not (default);
@@ -278,7 +278,8 @@ int qkn_last_launch(qkn_launch_info* info);
  *                    number of tokens, 0 = use the full grid (default);
  *   "token_blocks"   1 = each wavefront takes a contiguous range of tokens,
  *                    0 = tokens strided by the wavefront count (default);
- *   "waves_per_block" 1..4, 0 = automatic;
+ *   "waves_per_block" 1..4, 0 = automatic (register path: 1 for bf16,
+ *                    4 for fp8; wide path: always 4);
  *   "force_generic"  1 = always take the general path (same results);
  *   "validate_only"  1 = entry points validate their arguments and choose a
  *                    kernel (reported by qkn_last_launch, grid 0) but make no

@@ -57,8 +57,8 @@ constexpr int kWave = 64;
 constexpr int kMaxFastTp = kWave;   // one statistic slot per lane
 constexpr int kMaxStageBytes = 64 * 1024;
 // Grid sizing of the register path (measured on MI355X: HBM throughput peaks
-// with few, long-lived wavefronts per CU rather than full occupancy).
-constexpr int64_t kInFlightBytes = 24 * 1024;
+// with few, long-lived wavefronts per CU rather than full occupancy); the
+// rows requested per CU at a time are set per activation format below.
 constexpr int64_t kMinWavesPerCu = 6;
 
 // kFusedWait: fused, with the other ranks' statistics published concurrently
@@ -844,14 +844,22 @@ enum Format { kBf16 = 0, kFp8 = 1 };
 // itself: 8 bf16 chunks (d_local <= 4096) or 4 fp8 chunks (d_local <= 4096)
 // per tensor take the same registers. The wide path keeps only the packed rows
 // (slot 0 up to 32 bf16 / 16 fp8 chunks per lane, slot 1 as the register path).
+//
+// Register-path grid (measured on MI355X, prefill shards of 8192 and 32768
+// tokens): bf16 peaks with about 24 KB of rows requested per CU in one-wave
+// workgroups; fp8 rows are half as long and need more of them in flight,
+// about 32 KB per CU, best spread in four-wave workgroups.
 struct FormatInfo {
-  int esz;             // bytes per element
-  int per;             // elements per 16-byte chunk
-  int reg_max;         // register path: chunks per lane
-  int wide_n0[2];      // wide path: chunks per lane of the kernels for slot 0
-  const char* suffix;  // kernel-family suffix in launch names
+  int esz;                 // bytes per element
+  int per;                 // elements per 16-byte chunk
+  int reg_max;             // register path: chunks per lane
+  int wide_n0[2];          // wide path: chunks per lane of the kernels for slot 0
+  const char* suffix;      // kernel-family suffix in launch names
+  int64_t inflight_bytes;  // register path: row bytes to keep requested per CU
+  int waves_per_block;     // register path: default workgroup size in wavefronts
 };
-constexpr FormatInfo kFormat[2] = {{2, 8, 8, {16, 32}, ""}, {1, 16, 4, {8, 16}, "_fp8"}};
+constexpr FormatInfo kFormat[2] = {{2, 8, 8, {16, 32}, "", 24 * 1024, 1},
+                                   {1, 16, 4, {8, 16}, "_fp8", 32 * 1024, 4}};
 
 // Chunks per lane are rounded up to 1, 2, 4 or 8; unused chunks are masked.
 constexpr int kNIdx[9] = {-1, 0, 1, 2, 2, 3, 3, 3, 3};  // chunks/lane -> table index
@@ -1262,20 +1270,32 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
   int rc = query_device(&dev, &cus);
   if (rc != QKN_OK) return rc;
   int wpb = 1;
-  if (fast && !waits && g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
+  if (fast && !waits) {
+    // multi-wave workgroups only when the tokens fill every CU several times
+    // over; short launches (decode) spread one-wave workgroups over more CUs
+    if (g_opt_waves_per_block > 0) wpb = static_cast<int>(g_opt_waves_per_block);
+    else if (T >= static_cast<int64_t>(cus) * fi.waves_per_block * kMinWavesPerCu)
+      wpb = fi.waves_per_block;
+  }
   if (wide) wpb = 4;  // four wavefronts share the gamma staged in LDS
   const int block = wpb * kWave;
   int bpc = 0;
   rc = blocks_per_cu(dev, fn, block, lds, &bpc);
   if (rc != QKN_OK) return rc;
-  // Persistent grid: enough wavefronts per CU to keep about kInFlightBytes of
-  // rows requested per CU, at least kMinWavesPerCu, at most what fits.
+  // Persistent grid: enough wavefronts per CU to keep about fi.inflight_bytes
+  // of rows requested per CU, at least kMinWavesPerCu, at most what fits.
   int64_t waves_per_cu = static_cast<int64_t>(bpc) * wpb;
   if ((fast || wide) && mode != kFusedWait) {  // a waiting launch keeps every resident slot
     int64_t token_bytes = 0;
     for (int i = 0; i < nseg; ++i) token_bytes += fi.esz * static_cast<int64_t>(kp.seg[i].d);
-    int64_t want = (kInFlightBytes + token_bytes - 1) / token_bytes;
+    int64_t want = (fi.inflight_bytes + token_bytes - 1) / token_bytes;
     if (want < kMinWavesPerCu) want = kMinWavesPerCu;
+    // whole workgroups per CU: the dispatcher deals workgroups out evenly over
+    // the XCDs and their CUs, so a grid that is not a multiple of the CU count
+    // leaves some CUs with one workgroup more than others (measured: 13 waves
+    // per CU in 4-wave workgroups runs 15 % slower than 12)
+    want = (want + wpb / 2) / wpb * wpb;
+    if (want < wpb) want = wpb;
     if (want < waves_per_cu) waves_per_cu = want;
   }
   if (g_opt_waves_per_cu > 0) waves_per_cu = g_opt_waves_per_cu;
