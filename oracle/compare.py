@@ -131,3 +131,61 @@ def check_fp8(test: np.ndarray, ref: np.ndarray, what: str, noise: float = FP8_N
             f"{what}: FP8 result {t[i]!r} is not the rounding of oracle {r[i]!r} "
             f"at {idx.tolist()} (error {err[i]:.3e} > {bound[i]:.3e})")
     return float(np.max(err / half))
+
+
+# ---------------------------------------------------------------- projection
+
+FP32_UNIT = 2.0 ** -24  # unit roundoff of fp32
+
+
+def bf16_step(mag: np.ndarray) -> np.ndarray:
+    """bf16 grid step at magnitude `mag` (>= 0): 2^(e-7) in the binade
+    [2^e, 2^(e+1)), e >= -126; the subnormal step 2^-133 below."""
+    mag = np.asarray(mag, dtype=np.float64)
+    k = np.frexp(np.where(mag > 0, mag, 1.0))[1] - 1
+    k = np.where(mag > 0, np.maximum(k, -126), -126)
+    return np.exp2(k - 7.0)
+
+
+def projection_error_bound(q_exact: np.ndarray, dot_abs: np.ndarray, hidden: int) -> np.ndarray:
+    """Largest |q_stored - q_exact| for q accumulated in fp32 (any order) over
+    `hidden` exact bf16 products, then rounded once to bf16:
+    eps = (hidden - 1) u sum|x w| for the sum (to first order, padded by 1 %),
+    plus half a bf16 step at |q| + eps for the rounding."""
+    eps = 1.01 * max(hidden - 1, 0) * FP32_UNIT * np.asarray(dot_abs, dtype=np.float64)
+    return 0.5 * bf16_step(np.abs(q_exact) + eps) + eps
+
+
+def check_projection(q_test: np.ndarray, q_exact: np.ndarray, dot_abs: np.ndarray,
+                     hidden: int, what: str) -> float:
+    """Assert |q_test - q_exact| <= projection_error_bound elementwise; returns
+    the largest error as a fraction of its bound."""
+    q_test = np.asarray(q_test, dtype=np.float64)
+    q_exact = np.asarray(q_exact, dtype=np.float64)
+    if q_test.shape != q_exact.shape:
+        raise AssertionError(f"{what}: shape {q_test.shape} != {q_exact.shape}")
+    if not np.isfinite(q_test).all():
+        raise AssertionError(f"{what}: non-finite results")
+    bound = projection_error_bound(q_exact, dot_abs, hidden)
+    err = np.abs(q_test - q_exact)
+    frac = np.where(bound > 0, err / np.where(bound > 0, bound, 1.0), np.where(err > 0, np.inf, 0.0))
+    worst = float(frac.max()) if frac.size else 0.0
+    if not worst <= 1.0:
+        idx = np.unravel_index(int(np.argmax(frac)), frac.shape)
+        raise AssertionError(f"{what}: |q - exact| = {err[idx]:.3e} > bound {bound[idx]:.3e} at "
+                             f"{list(idx)} (q {q_test[idx]!r}, exact {q_exact[idx]!r})")
+    return worst
+
+
+def projection_partial_bound(q_exact: np.ndarray, dot_abs: np.ndarray, hidden: int) -> np.ndarray:
+    """Largest |P_test - sum_j round_bf16(q_exact)^2| per token, where P_test is
+    an fp32 sum of the squares of the stored values: each stored value differs
+    from the correctly rounded one by at most delta = one bf16 step at |q| + eps
+    plus eps; squares then differ by at most delta (2 |q| + 2 delta); the fp32
+    sum of d squares adds at most d u of the total (padded by 1 %)."""
+    q = np.abs(np.asarray(q_exact, dtype=np.float64))
+    eps = 1.01 * max(hidden - 1, 0) * FP32_UNIT * np.asarray(dot_abs, dtype=np.float64)
+    delta = bf16_step(q + eps) + eps
+    d = q.shape[1]
+    top = q + delta
+    return np.sum(delta * (2 * q + 2 * delta), axis=1) + 1.01 * d * FP32_UNIT * np.sum(top * top, axis=1)

@@ -44,6 +44,7 @@ import numpy as np
 BLOCK_TOKENS = 1024
 
 STREAM_XQ, STREAM_XK, STREAM_SCALE, STREAM_OUTLIER, STREAM_GQ, STREAM_GK = range(6)
+STREAM_PROJ_X, STREAM_PROJ_WQ, STREAM_PROJ_WK = 6, 7, 8
 
 
 @dataclass(frozen=True)
@@ -248,3 +249,39 @@ def random_rows(seed: int, T: int, d: int, dist: str = "normal", scale: float = 
 
 def random_gamma(seed: int, d: int) -> np.ndarray:
     return _rng(seed, 101).uniform(0.5, 1.5, size=d).astype(np.float32)
+
+
+# ------------------------------------------------------------------ projection inputs
+#
+# Inputs of the column-parallel Q/K projection that produces the activations
+# (Sec. II-B): the layer input x [T, hidden] and the full projection weights
+# W_Q [q_full, hidden], W_K [k_full, hidden] (a linear layer's out x in
+# layout; rank r's slice is rows shard_cols(...) of each). Recipe: x ~ N(0, 1)
+# drawn in 1024-token blocks from SeedSequence([seed, 6, block]); W_Q and W_K ~
+# N(0, 1/hidden) from streams 7 and 8 (so each projected value has unit
+# variance); all rounded to bf16 (RNE). The model width `hidden` is the Q
+# width of the workload unless given.
+
+def projection_inputs(wl: Workload, hidden: int = 0) -> Dict[str, np.ndarray]:
+    """``x`` uint16 [T, hidden], ``wq`` uint16 [q_full, hidden], ``wk`` uint16
+    [k_full, hidden] (bf16 bits)."""
+    hidden = hidden or wl.q_full
+    T = wl.T
+    x = np.empty((T, hidden), dtype=np.uint16)
+
+    def block(b: int) -> None:
+        t0, t1 = b * BLOCK_TOKENS, min(T, (b + 1) * BLOCK_TOKENS)
+        rng = np.random.default_rng(np.random.SeedSequence([wl.seed, STREAM_PROJ_X, b]))
+        x[t0:t1] = f32_to_bf16_bits(rng.standard_normal(size=(t1 - t0, hidden), dtype=np.float32))
+
+    nblocks = (T + BLOCK_TOKENS - 1) // BLOCK_TOKENS
+    if nblocks <= 1:
+        for b in range(nblocks):
+            block(b)
+    else:
+        with ThreadPoolExecutor(min(_threads(), nblocks)) as ex:
+            list(ex.map(block, range(nblocks)))
+    scale = np.float32(1.0 / np.sqrt(hidden))
+    wq = _rng(wl.seed, STREAM_PROJ_WQ).standard_normal(size=(wl.q_full, hidden), dtype=np.float32)
+    wk = _rng(wl.seed, STREAM_PROJ_WK).standard_normal(size=(wl.k_full, hidden), dtype=np.float32)
+    return {"x": x, "wq": f32_to_bf16_bits(wq * scale), "wk": f32_to_bf16_bits(wk * scale)}
