@@ -1,0 +1,91 @@
+/*
+ * qkn_proj.h -- C ABI of libqkn, part 2: the column-parallel Q/K projection
+ * with Phase A in its epilogue (AMD MI355X, gfx950).
+ *
+ * Under tensor parallelism the first projection of attention is split along
+ * its output dimension (Sec. II-B of SwiftQK, arXiv 2608.09160): rank r holds
+ * rows [r*d_local, (r+1)*d_local) of each weight W (a linear layer's
+ * out x in layout) and computes its slice of the projected activations from
+ * the full layer input x. Layerwise QK-Norm then needs, per token, the sum of
+ * squares of that slice (Phase A, Sec. III-A, Alg. 1). This entry point forms
+ * both in one pass over the projection's output tiles: the statistic is taken
+ * while the tile is still on chip, so Phase B (the exchange and the factor)
+ * and Phase C need no separate Phase A read (`qkn_apply` consumes them).
+ *
+ *   y[t, j]     = bf16( sum_k x[t, k] * W[j, k] )      fp32 accumulation,
+ *                                                     one rounding to nearest even
+ *   partials[t] = sum_j y[t, j]^2                      fp32, of the stored bf16 values
+ *
+ * Conventions are those of qkn.h (device pointers owned by the caller, bf16 as
+ * uint16_t bits, asynchronous on `stream`, validation before any HIP call,
+ * negative status codes, T == 0 a no-op).
+ *
+ * Summation tree of partials[t] (fixed; depends only on d_local): the columns
+ * are taken in tiles of 128; within a tile, two fused-multiply-add chains in
+ * ascending column order over columns [0, 64) and [64, 128) of the tile, added
+ * (first + second); the tile sums are then added in ascending tile order.
+ * Results are deterministic and independent of the launch shape; they are
+ * not bit-identical to qkn_partial_sumsq of y, whose tree differs (both are
+ * fp32 sums of the same squares).
+ */
+#ifndef QKN_PROJ_H
+#define QKN_PROJ_H
+
+#include <stdint.h>
+
+#include "qkn.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * One projection output (Q or K) of one rank.
+ *   w        bf16 [d_local, ldw], the rank's rows of the weight; columns
+ *            [0, hidden) are used; ldw >= hidden.
+ *   y        bf16 [T, ldy] output, columns [0, d_local); ldy >= d_local.
+ *   partials fp32 [T] output: the Phase A statistic of y's rows.
+ *   d_local  rows of w = columns of y (>= 1).
+ */
+typedef struct qkn_proj_seg {
+  const uint16_t* w;
+  int64_t ldw;
+  uint16_t* y;
+  int64_t ldy;
+  float* partials;
+  int64_t d_local;
+} qkn_proj_seg;
+
+/*
+ * Bytes of device workspace qkn_proj_partial needs for these segments and T
+ * tokens (the per-tile statistics before they are added in tile order):
+ * 4 * T * sum over segments of ceil(d_local / 128). Returns a negative status
+ * for invalid arguments (segs NULL, nseg not 1 or 2, T < 0, d_local < 1).
+ */
+int64_t qkn_proj_workspace_bytes(int64_t T, const qkn_proj_seg* segs, int nseg);
+
+/*
+ * Projection of the layer input x (bf16 [T, ldx], columns [0, hidden)) onto
+ * 1 or 2 weight slices (Q and K of the same tokens) in one launch, each
+ * output tile's Phase A statistic taken in the epilogue, then the tile
+ * statistics added in a second, small launch.
+ *   workspace  device memory of at least qkn_proj_workspace_bytes(...) bytes,
+ *              16-byte aligned; its contents on entry do not matter.
+ * Requirements of the MFMA path (else QKN_ENOTSUP): x, every w and y 16-byte
+ * aligned; hidden, ldx, ldw, ldy and d_local multiples of 8; T * ldx * 2 and
+ * d_local * ldw * 2 below 2^31 bytes.
+ * QKN_EINVAL: x NULL with T > 0, T < 0, hidden < 1, ldx < hidden, segs NULL,
+ * nseg not 1 or 2, a segment with NULL w/y/partials, d_local < 1,
+ * ldw < hidden, ldy < d_local, workspace NULL or smaller than required.
+ * QKN_EOVERLAP: an output (y, partials, workspace) overlapping an input or
+ * another output.
+ */
+int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
+                     const qkn_proj_seg* segs, int nseg, void* workspace,
+                     int64_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QKN_PROJ_H */

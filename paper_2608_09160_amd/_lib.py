@@ -35,6 +35,11 @@ class QknSeg(ctypes.Structure):
                 ("d_local", _c_i64), ("d_full", _c_i64)]
 
 
+class QknProjSeg(ctypes.Structure):
+    _fields_ = [("w", _vp), ("ldw", _c_i64), ("y", _vp), ("ldy", _c_i64), ("partials", _vp),
+                ("d_local", _c_i64)]
+
+
 class QknWait(ctypes.Structure):
     _fields_ = [("slots", _vp * 2), ("epoch", ctypes.c_uint32), ("spin_limit", _c_i64),
                 ("co_resident", ctypes.c_int), ("status", _vp)]
@@ -79,6 +84,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qkn_apply_fp8.argtypes = lib.qkn_apply.argtypes
     lib.qkn_fused_shard_fp8.argtypes = lib.qkn_fused_shard.argtypes
     lib.qkn_full_fp8.argtypes = lib.qkn_full.argtypes
+    lib.qkn_proj_workspace_bytes.argtypes = [_c_i64, ctypes.POINTER(QknProjSeg), ctypes.c_int]
+    lib.qkn_proj_workspace_bytes.restype = _c_i64
+    lib.qkn_proj_partial.argtypes = [_vp, _c_i64, _c_i64, _c_i64, ctypes.POINTER(QknProjSeg),
+                                     ctypes.c_int, _vp, _c_i64, _vp]
     lib.qkn_strerror.argtypes = [ctypes.c_int]
     lib.qkn_strerror.restype = ctypes.c_char_p
     lib.qkn_last_launch.argtypes = [ctypes.POINTER(QknLaunchInfo)]
@@ -86,7 +95,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
                  "qkn_last_launch", "qkn_set_option", "qkn_publish_partials",
                  "qkn_fused_shard_wait", "qkn_fused_group_wait", "qkn_partial_sumsq_fp8",
-                 "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8"):
+                 "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8", "qkn_proj_partial"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -356,6 +365,80 @@ class Prepared:
         else:
             rc = self._fn(self._arr, self._n, self._tp, self._rank, self._T, self._eps, st)
         _check(rc, self.name)
+
+
+@dataclass
+class ProjSeg:
+    """One projection output (Q or K) of one rank for qkn_proj_partial."""
+
+    w: torch.Tensor                         # bf16 [d_local, hidden] (row stride free)
+    y: Optional[torch.Tensor] = None        # bf16 [T, d_local]; allocated if None
+    partials: Optional[torch.Tensor] = None  # fp32 [T]; allocated if None
+
+
+def _proj_segs(segs: Sequence[ProjSeg], T: int, hidden: int, device):
+    arr = (QknProjSeg * len(segs))()
+    for i, s in enumerate(segs):
+        pw, ldw, d, hw = _rows(s.w, f"seg{i}.w")
+        if hw != hidden:
+            raise ValueError(f"seg{i}.w: expected {hidden} columns, got {hw}")
+        if s.y is None:
+            s.y = torch.empty((T, d), dtype=torch.bfloat16, device=device)
+        py, ldy, Ty, dy = _rows(s.y, f"seg{i}.y")
+        if (Ty, dy) != (T, d):
+            raise ValueError(f"seg{i}.y: expected [{T}, {d}], got {tuple(s.y.shape)}")
+        if s.partials is None:
+            s.partials = torch.empty(T, dtype=torch.float32, device=device)
+        arr[i] = QknProjSeg(pw, ldw, py, ldy, _f32(s.partials, f"seg{i}.partials", T), d)
+    return arr
+
+
+def qkn_proj_workspace_bytes(T: int, segs: Sequence[ProjSeg]) -> int:
+    arr = (QknProjSeg * len(segs))()
+    for i, s in enumerate(segs):
+        arr[i] = QknProjSeg(None, 0, None, 0, None, s.w.shape[0])
+    n = load().qkn_proj_workspace_bytes(T, arr, len(segs))
+    if n < 0:
+        raise QknError(int(n), "qkn_proj_workspace_bytes")
+    return int(n)
+
+
+def qkn_proj_partial(x: torch.Tensor, segs: Sequence[ProjSeg],
+                     workspace: Optional[torch.Tensor] = None, stream=None):
+    """y = bf16(x @ w^T) per segment and its Phase A statistic (fp32 [T]).
+
+    x: bf16 [T, hidden]; workspace: a uint8 GPU tensor of at least
+    qkn_proj_workspace_bytes bytes (allocated if None). Returns the segments'
+    (y, partials) pairs.
+    """
+    px, ldx, T, hidden = _rows(x, "x")
+    arr = _proj_segs(segs, T, hidden, x.device)
+    need = qkn_proj_workspace_bytes(T, segs)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace: expected a contiguous uint8 GPU tensor")
+    _check(load().qkn_proj_partial(px, ldx, T, hidden, arr, len(segs), workspace.data_ptr(),
+                                   workspace.numel(), _stream(stream)), "qkn_proj_partial")
+    return [(s.y, s.partials) for s in segs]
+
+
+class PreparedProj:
+    """qkn_proj_partial with its argument block and workspace prepared once."""
+
+    def __init__(self, x: torch.Tensor, segs: Sequence[ProjSeg]):
+        self.x, self.segs = x, list(segs)
+        self._px, self._ldx, self._T, self._hidden = _rows(x, "x")
+        self._arr = _proj_segs(self.segs, self._T, self._hidden, x.device)
+        need = qkn_proj_workspace_bytes(self._T, self.segs)
+        self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
+        self._lib = load()
+
+    def __call__(self, stream=None) -> None:
+        _check(self._lib.qkn_proj_partial(self._px, self._ldx, self._T, self._hidden, self._arr,
+                                          len(self.segs), self.workspace.data_ptr(),
+                                          self.workspace.numel(), _stream(stream)),
+               "qkn_proj_partial")
 
 
 def qkn_last_launch() -> dict:

@@ -3,8 +3,9 @@
     python -m paper_2608_09160_amd.build [--asm]
 
 The library is written to this package's directory so that it travels with
-the source tree. `--asm` also writes the gfx950 assembly next to it
-(libqkn-gfx950.s) for inspection of register use and instruction selection.
+the source tree. `--asm` also writes the gfx950 assembly of each source next
+to it (libqkn-<source>-gfx950.s) for inspection of register use and
+instruction selection.
 """
 from __future__ import annotations
 
@@ -14,7 +15,7 @@ import sys
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG_DIR)
-SRC = os.path.join(PKG_DIR, "csrc", "qkn.hip")
+SOURCES = [os.path.join(PKG_DIR, "csrc", name) for name in ("qkn.hip", "qkn_proj.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG_DIR, "libqkn.so")
 ARCH = "gfx950"
@@ -41,13 +42,15 @@ def _run(cmd):
 def build(asm: bool = False, verbose: bool = False) -> str:
     """Compile libqkn.so (always recompiles). Returns the library path."""
     tmp = LIB + ".tmp"
-    out = _run([HIPCC, *COMMON, "-shared", "-fPIC", "-o", tmp, SRC])
+    out = _run([HIPCC, *COMMON, "-shared", "-fPIC", "-o", tmp, *SOURCES])
     os.replace(tmp, LIB)
     if verbose and out.strip():
         print(out)
     if asm:
-        _run([HIPCC, *COMMON, "--cuda-device-only", "-S", "-o",
-              os.path.join(PKG_DIR, f"libqkn-{ARCH}.s"), SRC])
+        for src in SOURCES:
+            stem = os.path.splitext(os.path.basename(src))[0]
+            _run([HIPCC, *COMMON, "--cuda-device-only", "-S", "-o",
+                  os.path.join(PKG_DIR, f"libqkn-{stem}-{ARCH}.s"), src])
     return LIB
 
 

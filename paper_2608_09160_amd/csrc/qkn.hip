@@ -45,8 +45,12 @@
 #include <mutex>
 
 #include "qkn.h"
+#include "qkn_host.h"
 
 namespace {
+
+using qkn_host::Span;
+using qkn_host::spans_overlap;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -1033,40 +1037,6 @@ HSeg to_hseg(const S& s) {
 
 bool bad_eps(float eps) { return !(eps >= 0.0f) || !isfinite(eps); }
 
-// A strided byte region: `rows` rows of `width` elements every `ld` elements.
-struct Span {
-  uintptr_t base;
-  int64_t rows, ld, width, esz;
-};
-
-int64_t floor_div(int64_t a, int64_t b) {  // b > 0
-  int64_t q = a / b;
-  if ((a % b != 0) && ((a < 0) != (b < 0))) --q;
-  return q;
-}
-
-bool spans_overlap(const Span& a, const Span& b) {
-  if (a.rows <= 0 || b.rows <= 0 || a.width <= 0 || b.width <= 0) return false;
-  const __int128 a_lo = a.base, b_lo = b.base;
-  const __int128 a_hi = a_lo + ((__int128)(a.rows - 1) * a.ld + a.width) * a.esz;
-  const __int128 b_hi = b_lo + ((__int128)(b.rows - 1) * b.ld + b.width) * b.esz;
-  if (a_hi <= b_lo || b_hi <= a_lo) return false;  // disjoint extents
-  // Same element size and stride: exact test on element offsets.
-  if (a.esz == b.esz && a.ld == b.ld && a.ld > 0) {
-    const __int128 off_bytes = b_lo - a_lo;
-    if (off_bytes % a.esz == 0) {
-      const int64_t o = static_cast<int64_t>(off_bytes / a.esz);
-      const int64_t ld = a.ld;
-      // rows r of a and s of b overlap iff o - wa < (r - s) * ld < o + wb
-      const int64_t dmin = -(b.rows - 1), dmax = a.rows - 1;
-      int64_t d = floor_div(o - a.width, ld) + 1;
-      if (d < dmin) d = dmin;
-      return d <= dmax && (__int128)d * ld < (__int128)o + b.width;
-    }
-  }
-  return true;  // conservative
-}
-
 Span elem_span(const void* p, int64_t rows, int64_t ld, int64_t width, int esz) {
   return Span{reinterpret_cast<uintptr_t>(p), rows, ld, width, esz};
 }
@@ -1418,6 +1388,11 @@ int full_entry(const S* segs, int nseg, int64_t T, float eps, int fmt, void* str
 }
 
 }  // namespace
+
+namespace qkn_host {
+bool validate_only() { return g_opt_validate_only != 0; }
+void record_launch(const qkn_launch_info& info) { t_last = info; }
+}  // namespace qkn_host
 
 extern "C" {
 

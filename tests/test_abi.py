@@ -34,7 +34,8 @@ def dry(lib):
 
 
 def _declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(os.path.join(os.path.dirname(HEADER), h)).read()
+                   for h in sorted(os.listdir(os.path.dirname(HEADER))) if h.endswith(".h"))
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(qkn_[a-z0-9_]+)\s*\(", text)))
 
@@ -44,7 +45,7 @@ def test_header_symbols_exported(lib):
     assert set(names) >= {"qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
                           "qkn_strerror", "qkn_last_launch", "qkn_set_option",
                           "qkn_partial_sumsq_fp8", "qkn_apply_fp8", "qkn_fused_shard_fp8",
-                          "qkn_full_fp8"}
+                          "qkn_full_fp8", "qkn_proj_workspace_bytes", "qkn_proj_partial"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -287,7 +288,7 @@ def test_struct_layouts_match_header(tmp_path):
     src = tmp_path / "layout.c"
     src.write_text('''#include <stdio.h>
 #include <stddef.h>
-#include "qkn.h"
+#include "qkn_proj.h"
 #define F(T, m) printf(#T "." #m " %zu\\n", offsetof(T, m))
 int main(void) {
   printf("qkn_seg %zu\\n", sizeof(qkn_seg)); F(qkn_seg, x); F(qkn_seg, ldx); F(qkn_seg, w);
@@ -296,6 +297,8 @@ int main(void) {
   printf("qkn_seg8 %zu\\n", sizeof(qkn_seg8)); F(qkn_seg8, x); F(qkn_seg8, ldx); F(qkn_seg8, w);
   F(qkn_seg8, partials); F(qkn_seg8, y); F(qkn_seg8, ldy); F(qkn_seg8, inv_rms);
   F(qkn_seg8, d_local); F(qkn_seg8, d_full);
+  printf("qkn_proj_seg %zu\\n", sizeof(qkn_proj_seg)); F(qkn_proj_seg, w); F(qkn_proj_seg, ldw);
+  F(qkn_proj_seg, y); F(qkn_proj_seg, ldy); F(qkn_proj_seg, partials); F(qkn_proj_seg, d_local);
   printf("qkn_wait %zu\\n", sizeof(qkn_wait)); F(qkn_wait, slots); F(qkn_wait, epoch);
   F(qkn_wait, spin_limit); F(qkn_wait, co_resident); F(qkn_wait, status);
   printf("qkn_launch_info %zu\\n", sizeof(qkn_launch_info)); F(qkn_launch_info, kernel);
@@ -310,7 +313,8 @@ int main(void) {
     c = dict(line.rsplit(" ", 1) for line in
              subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
              if line)
-    for name, cls in (("qkn_seg", L.QknSeg), ("qkn_seg8", L.QknSeg), ("qkn_wait", L.QknWait),
+    for name, cls in (("qkn_seg", L.QknSeg), ("qkn_seg8", L.QknSeg), ("qkn_proj_seg", L.QknProjSeg),
+                      ("qkn_wait", L.QknWait),
                       ("qkn_launch_info", L.QknLaunchInfo)):
         assert int(c[name]) == ctypes.sizeof(cls), name
         for field, _ in cls._fields_:
@@ -473,3 +477,65 @@ def test_fp8_alignment_and_overlap_in_bytes(dry):
     # in place is allowed
     seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, x, 1024, 1024, 2048)
     assert _fused8(dry, [seg], 2, 0, T) == 0
+
+
+# ------------------------------------------------------------------ projection
+
+def _pseg(w, ldw, y, ldy, partials, d):
+    return L.QknProjSeg(w, ldw, y, ldy, partials, d)
+
+
+def _proj(lib, x, ldx, T, hidden, segs, ws, ws_bytes):
+    arr = (L.QknProjSeg * len(segs))(*segs)
+    return lib.qkn_proj_partial(x, ldx, T, hidden, arr, len(segs), ws, ws_bytes, None)
+
+
+def test_proj_workspace_size(lib):
+    segs = (L.QknProjSeg * 2)(_pseg(0, 0, 0, 0, 0, 2048), _pseg(0, 0, 0, 0, 0, 520))
+    assert lib.qkn_proj_workspace_bytes(8192, segs, 2) == 4 * 8192 * (16 + 5)
+    assert lib.qkn_proj_workspace_bytes(8192, segs, 1) == 4 * 8192 * 16
+    assert lib.qkn_proj_workspace_bytes(-1, segs, 1) == L.QKN_EINVAL
+    assert lib.qkn_proj_workspace_bytes(8, segs, 3) == L.QKN_EINVAL
+    bad = (L.QknProjSeg * 1)(_pseg(0, 0, 0, 0, 0, 0))
+    assert lib.qkn_proj_workspace_bytes(8, bad, 1) == L.QKN_EINVAL
+
+
+def test_proj_validation(lib):
+    T, h = 300, 4096
+    X, W, Y, P, WS = BASE, BASE + 64 * MB, BASE + 128 * MB, BASE + 192 * MB, BASE + 200 * MB
+    ok = _pseg(W, h, Y, 2048, P, 2048)
+    need = 4 * T * 16
+    # T == 0 is a no-op even with NULL pointers
+    assert _proj(lib, None, h, 0, h, [ok], None, 0) == 0
+    assert _proj(lib, X, h, T, h, [ok], WS, need - 4) == L.QKN_EINVAL          # workspace too small
+    assert _proj(lib, X, h, T, h, [ok], None, need) == L.QKN_EINVAL            # no workspace
+    assert _proj(lib, X, h - 8, T, h, [ok], WS, need) == L.QKN_EINVAL          # ldx < hidden
+    assert _proj(lib, X, h, T, h, [_pseg(W, h - 8, Y, 2048, P, 2048)], WS, need) == L.QKN_EINVAL
+    assert _proj(lib, X, h, T, h, [_pseg(W, h, Y, 2040, P, 2048)], WS, need) == L.QKN_EINVAL
+    assert _proj(lib, X, h, T, h, [_pseg(W, h, Y, 2048, None, 2048)], WS, need) == L.QKN_EINVAL
+    assert _proj(lib, X, h, T, h, [ok, ok, ok], WS, need) == L.QKN_EINVAL
+    # alignment and multiples of 8 (the MFMA path)
+    assert _proj(lib, X + 2, h, T, h, [ok], WS, need) == L.QKN_ENOTSUP
+    assert _proj(lib, X, h + 4, T, h, [ok], WS, need) == L.QKN_ENOTSUP
+    assert _proj(lib, X, 4100, T, 4100, [_pseg(W, 4100, Y, 2048, P, 2048)], WS, need) == L.QKN_ENOTSUP
+    assert _proj(lib, X, h, T, h, [_pseg(W, h, Y, 2048, P, 2044)], WS, need) == L.QKN_ENOTSUP
+    # overlaps: y onto x, partials onto y, workspace onto w; Q and K outputs as
+    # disjoint column slices of one buffer are fine
+    assert _proj(lib, X, h, T, h, [_pseg(W, h, X + 8192, 2048, P, 2048)], WS, need) == L.QKN_EOVERLAP
+    assert _proj(lib, X, h, T, h, [_pseg(W, h, Y, 2048, Y + 64, 2048)], WS, need) == L.QKN_EOVERLAP
+    assert _proj(lib, X, h, T, h, [ok], W + 4096, need) == L.QKN_EOVERLAP
+    q = _pseg(W, h, Y, 2560, P, 2048)
+    k = _pseg(W + 32 * MB, h, Y + 2048 * 2, 2560, P + MB, 512)
+    need2 = 4 * T * (16 + 4)
+    assert dry_proj_ok(lib, X, h, T, h, [q, k], WS, need2)
+    k_bad = _pseg(W + 32 * MB, h, Y + 2040 * 2, 2560, P + MB, 512)
+    assert _proj(lib, X, h, T, h, [q, k_bad], WS, need2) == L.QKN_EOVERLAP
+
+
+def dry_proj_ok(lib, *args):
+    """Validation passes: with validate_only the call returns before any HIP call."""
+    assert lib.qkn_set_option(b"validate_only", 1) == 0
+    try:
+        return _proj(lib, *args) == 0
+    finally:
+        assert lib.qkn_set_option(b"validate_only", 0) == 0
