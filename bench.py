@@ -391,6 +391,40 @@ def summarize(outdir: str) -> None:
           f"bench kernel_us {bench['roofline']['kernel_us']}")
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+
+
+def proj_extra(torch, L, workloads, wl, rank, steps=50):
+    dev = "cuda:0"
+
+    def bf16(a):
+        a = np.ascontiguousarray(a, dtype=np.uint16)
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+    data = workloads.projection_inputs(wl)
+    x = bf16(data["x"])
+    wq = bf16(data["wq"][workloads.shard_cols(wl.q_full, wl.tp, rank)])
+    wk = bf16(data["wk"][workloads.shard_cols(wl.k_full, wl.tp, rank)])
+    hidden = x.shape[1]
+    flops = 2 * wl.T * hidden * (wq.shape[0] + wk.shape[0])
+    prep = L.PreparedProj(x, [L.ProjSeg(w=wq), L.ProjSeg(w=wk)])
+    wqk_t = torch.cat([wq, wk]).t().contiguous()
+    ours, lib = [], []
+    for _ in range(3):  # alternate, median of three regions each
+        ours.append(time_region(torch, lambda i: prep(), steps, 5) / steps)
+        lib.append(time_region(torch, lambda i: torch.mm(x, wqk_t), steps, 5) / steps)
+    prep()
+    info = L.qkn_last_launch()
+    t, tm = float(np.median(ours)), float(np.median(lib))
+    tf = flops / (t * 1e-3) / 1e12
+    return {"kernel": info["kernel"], "grid": info["grid"], "tokens": wl.T, "hidden": hidden,
+            "columns": wq.shape[0] + wk.shape[0], "flops": flops, "kernel_us": round(t * 1e3, 2),
+            "tflops": round(tf, 1), "roofline": {"bound": "mfma", "peak": MFMA_BF16_PEAK_TFLOPS,
+                                                  "unit": "TFLOP/s",
+                                                  "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+            "torch_mm_us": round(tm * 1e3, 2),
+            "torch_mm_tflops": round(flops / (tm * 1e-3) / 1e12, 1)}
+
+
 def cpu_baseline(wl, rank, data, seconds):
     """The fp64 oracle as it stands, on the host: bounded sample of the workload."""
     from oracle import qknorm as Q
@@ -540,6 +574,11 @@ def main():
                                               "kernel": L.qkn_last_launch()["kernel"],
                                               "bytes": d8.bytes}
         del d8
+        # Phase A in the Q/K projection's epilogue: the rank's column-parallel
+        # projection (hidden 4096 -> Q 2048 + K 512 columns) on the matrix
+        # cores, with the statistic taken from each output tile; against
+        # torch.mm (hipBLASLt) of the same product without the statistic
+        extras["proj_partial_prefill"] = proj_extra(torch, L, workloads, wl, args.rank)
         print("[bench] extras done", file=sys.stderr, flush=True)
 
     cpu = None

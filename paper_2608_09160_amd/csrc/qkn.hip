@@ -1583,6 +1583,8 @@ int qkn_set_option(const char* key, int64_t value) {
   } else if (strcmp(key, "token_blocks") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_token_blocks = value;
+  } else if (strcmp(key, "proj_tile") == 0) {
+    return qkn_host::set_proj_tile(value);
   } else if (strcmp(key, "validate_only") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_validate_only = value;

@@ -14,6 +14,9 @@ namespace qkn_host {
 // record it, but launch nothing. Defined in qkn.hip.
 __attribute__((visibility("hidden"))) bool validate_only();
 
+// The projection's tile-shape choice ("proj_tile" option). Defined in qkn_proj.hip.
+__attribute__((visibility("hidden"))) int set_proj_tile(int64_t choice);
+
 // Records the calling thread's latest launch for qkn_last_launch.
 __attribute__((visibility("hidden"))) void record_launch(const qkn_launch_info& info);
 

@@ -14,10 +14,14 @@
 //     column (l mod 32), rows 8*(r/4) + 4*(l/32) + (r mod 4) in accumulator r.
 //   * A 256-thread workgroup owns a 128 x 128 output tile (four wavefronts in
 //     2 x 2, 64 x 64 each = 2 x 2 MFMA blocks); k advances 64 at a time
-//     through two LDS stages: the next stage's global loads are issued before
-//     the current stage's MFMAs and written to the other LDS buffer after
-//     them, one barrier per stage. LDS rows are padded to 144 bytes, which
-//     spreads a 16-lane group's 16-byte reads over all 64 banks.
+//     through two LDS stages that global memory fills directly (buffer_load
+//     ... lds, no VGPR staging): the loads of stage kt + 1 are in flight while
+//     stage kt is computed, one barrier per stage. Instead of padding, each
+//     row's 16-byte k-slots are XOR-swizzled so that the 16 rows a 16-lane
+//     group reads land on 16 distinct bank groups. Two such workgroups (64 KB
+//     of LDS each) share a CU. (Measured on MI355X against register-staged
+//     double buffering, three- and four-stage rings, k of 32 and 128 per stage
+//     and 256-wide tiles: this shape was the fastest.)
 //   * Global loads are raw buffer loads whose descriptors end at the last
 //     valid row, so rows past T or d_local read zeros; the k tail (hidden not
 //     a multiple of 64) is masked by moving the offset out of range.
@@ -52,28 +56,27 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
-constexpr int kBM = 128;                  // output rows (tokens) per tile
-constexpr int kBN = 128;                  // output columns per tile
-constexpr int kBK = 64;                   // k per LDS stage
-constexpr int kThreads = 256;             // four wavefronts, 2 x 2 over the tile
-constexpr int kLdsRow = kBK + 8;          // bf16 per staged row (144 bytes)
-constexpr int kStage = kBM * kLdsRow;     // bf16 per staged operand tile
-constexpr int kOutRow = kBN + 8;          // bf16 per staged output row (272 bytes)
+// Output tiles: a 256-thread workgroup (four wavefronts, 2 x 2) owns
+// (64 WMB) x (64 WNB) outputs, each wavefront (32 WMB) x (32 WNB) as WMB x WNB
+// MFMA blocks; k advances BK per LDS stage. The Phase A statistic is always
+// taken over 128-column chunks of the output (kChunkN), whatever the tile
+// width, so its summation tree does not depend on the tile shape.
+constexpr int kThreads = 256;
+constexpr int kChunkN = 128;              // columns per statistic chunk
 constexpr int kGroupM = 8;                // row tiles per tile group
 constexpr int kXcds = 8;                  // MI355X: workgroup id mod 8 selects the XCD
 constexpr int kRsrcWord3 = 0x00020000;    // raw (untyped) buffer
-
-static_assert(kBM * kOutRow <= 4 * kStage, "the output tile reuses the operand stages");
+constexpr int kLdsBytes = 160 * 1024;     // LDS per CU on gfx950
 
 struct ProjSegDev {
   const uint16_t* w;
   uint16_t* y;
-  float* tile_partials;  // [ntiles, T]
+  float* tile_partials;  // [nchunks, T]: statistic of each 128-column chunk
   float* partials;       // [T]
   int64_t ldw, ldy;
   int32_t d;
   int32_t tile0;         // first column tile of this segment in the launch
-  int32_t ntiles;
+  int32_t nchunks;       // ceil(d / 128)
 };
 
 struct ProjParams {
@@ -127,16 +130,114 @@ __device__ __forceinline__ bool tile_of(int bid, int grid, const ProjParams& p, 
   return true;
 }
 
+// Epilogue of a (64 WMB) x (64 WNB) tile: round the fp32 accumulators once to
+// bf16, stage the tile in LDS (`lds`, at least BM x OUT_ROW bf16; the caller
+// has finished with it), write it to y with coalesced 16-byte stores, and
+// take the Phase A statistic of each row's 128-column chunks.
+template <int WMB, int WNB, int OUT_ROW>
+__device__ __forceinline__ void epilogue(const ProjParams& p, const ProjSegDev& s,
+                                         const f32x16 (&acc)[WMB][WNB], uint16_t* lds, int64_t m0,
+                                         int n0, int rows_a, int rows_b) {
+  constexpr int BM = 64 * WMB, BN = 64 * WNB;
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  uint16_t* out = lds;  // [BM][OUT_ROW]
+#pragma unroll
+  for (int i = 0; i < WMB; ++i)
+#pragma unroll
+    for (int j = 0; j < WNB; ++j) {
+      const int col = wn * 32 * WNB + j * 32 + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        const int row = wm * 32 * WMB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const uint32_t pk = pack_bf16x2(acc[i][j][r], acc[i][j][r + 1]);
+        out[row * OUT_ROW + col] = static_cast<uint16_t>(pk & 0xffffu);
+        out[(row + 1) * OUT_ROW + col] = static_cast<uint16_t>(pk >> 16);
+      }
+    }
+  __syncthreads();
+
+  // coalesced 16-byte stores of the tile rows (columns past d_local skipped)
+  const uint32_t y_bytes = static_cast<uint32_t>(rows_a * s.ldy * 2);
+  const Rsrc ry = make_rsrc(s.y + m0 * s.ldy + n0, y_bytes);
+  constexpr int kRowVecs = BN / 8;
+#pragma unroll
+  for (int i = 0; i < BM * kRowVecs / kThreads; ++i) {
+    const int v = tid + kThreads * i;
+    const int row = v / kRowVecs, cv = (v % kRowVecs) * 8;
+    const u32x4 val = *reinterpret_cast<const u32x4*>(out + row * OUT_ROW + cv);
+    st16(val, ry, cv < rows_b ? static_cast<uint32_t>((row * s.ldy + cv) * 2) : y_bytes);
+  }
+
+  // Phase A per 128-column chunk: thread pair (2u, 2u+1) takes one row of one
+  // chunk, columns [0, 64) and [64, 128) of it in ascending order; the pair adds.
+  constexpr int kUnits = BM * (BN / kChunkN) * 2;
+#pragma unroll
+  for (int it = 0; it < kUnits / kThreads; ++it) {
+    const int u = tid + kThreads * it;
+    const int half = u & 1, rc = u >> 1;
+    const int row = rc % BM, chunk = rc / BM;
+    const uint16_t* src = out + row * OUT_ROW + chunk * kChunkN + half * 64;
+    float acc_s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < 64; c += 8) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(src + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = bf16_lo(v[e]), hi = bf16_hi(v[e]);
+        acc_s = __builtin_fmaf(lo, lo, acc_s);
+        acc_s = __builtin_fmaf(hi, hi, acc_s);
+      }
+    }
+    // the partner lane's sum (quad_perm [1,0,3,2]: lanes 2u and 2u+1 swap)
+    const float other = __builtin_bit_cast(
+        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc_s), 0xB1, 0xF, 0xF, false));
+    const float first = half ? other : acc_s;
+    const float second = half ? acc_s : other;
+    const float chunk_sum = first + second;
+    const int gchunk = n0 / kChunkN + chunk;  // chunk index within the segment
+    if (half == 0 && row < rows_a && gchunk < s.nchunks)
+      s.tile_partials[static_cast<int64_t>(gchunk) * p.T + m0 + row] = chunk_sum;
+  }
+}
+
+template <int WMB, int WNB, int BK>
+struct TileCfg {
+  static constexpr int BM = 64 * WMB;                 // tile rows (tokens)
+  static constexpr int BN = 64 * WNB;                 // tile columns
+  static constexpr int kRow = BK + 8;                 // bf16 per staged operand row (padded)
+  static constexpr int kStageA = BM * kRow;
+  static constexpr int kStage = (BM + BN) * kRow;     // bf16 per LDS stage (A then B)
+  static constexpr int kOutRow = BN + 8;              // bf16 per staged output row
+  static constexpr int kLds = (2 * kStage > BM * kOutRow) ? 2 * kStage : BM * kOutRow;
+  static constexpr int kKv = BK / 8;                  // 16-byte vectors per operand row
+  static constexpr int kVecA = BM * kKv / kThreads;   // per thread per stage
+  static constexpr int kVecB = BN * kKv / kThreads;
+  static_assert(BM * kKv % kThreads == 0 && BN * kKv % kThreads == 0, "whole vectors per thread");
+  static_assert(BN % kChunkN == 0, "tiles hold whole statistic chunks");
+  static_assert(kLds * 2 <= kLdsBytes, "LDS");
+};
+
+// Register-staged kernel: each stage's operand tiles go global -> VGPRs ->
+// LDS (rows padded to BK + 8 bf16, which spreads a 16-lane group's 16-byte
+// reads over all 64 banks); the next stage's loads are issued before the
+// current stage's MFMAs and written to the other LDS buffer after them. Kept as
+// a second, independently staged implementation: it must give the same bits
+// as the direct-to-LDS kernel (the k order of every accumulation is the same).
+template <int WMB, int WNB, int BK>
 __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
-  __shared__ __align__(16) uint16_t lds[4 * kStage];  // [stage][A, B][row][k]
+  using C = TileCfg<WMB, WNB, BK>;
+  __shared__ __align__(16) uint16_t lds[C::kLds];
   int mt, nt;
   if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p, mt, nt)) return;
   const int si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
   const ProjSegDev& s = p.seg[si];
-  const int64_t m0 = static_cast<int64_t>(mt) * kBM;
-  const int n0 = (nt - s.tile0) * kBN;
-  const int rows_a = static_cast<int>((p.T - m0 < kBM) ? p.T - m0 : kBM);
-  const int rows_b = (s.d - n0 < kBN) ? s.d - n0 : kBN;
+  const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
+  const int n0 = (nt - s.tile0) * C::BN;
+  const int rows_a = static_cast<int>((p.T - m0 < C::BM) ? p.T - m0 : C::BM);
+  const int rows_b = (s.d - n0 < C::BN) ? s.d - n0 : C::BN;
 
   const int tid = static_cast<int>(threadIdx.x);
   const int lane = tid & 63;
@@ -149,38 +250,182 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
   const Rsrc ra = make_rsrc(p.x + m0 * p.ldx, a_bytes);
   const Rsrc rb = make_rsrc(s.w + static_cast<int64_t>(n0) * s.ldw, b_bytes);
 
-  // this thread's four 16-byte vectors of each operand tile per stage
-  uint32_t a_row_off[4], b_row_off[4];
-  int lds_off[4];
-  int kv8[4];
+  // this thread's 16-byte vectors of each operand tile per stage
+  uint32_t a_off[C::kVecA], b_off[C::kVecB];
+  int a_lds[C::kVecA], b_lds[C::kVecB], a_k[C::kVecA], b_k[C::kVecB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < C::kVecA; ++i) {
     const int v = tid + kThreads * i;
-    const int row = v >> 3, kv = v & 7;
-    a_row_off[i] = static_cast<uint32_t>(row * p.ldx * 2);
-    b_row_off[i] = static_cast<uint32_t>(row * s.ldw * 2);
-    lds_off[i] = row * kLdsRow + kv * 8;
-    kv8[i] = kv * 8;
+    const int row = v / C::kKv, kv = v % C::kKv;
+    a_off[i] = static_cast<uint32_t>(row * p.ldx * 2);
+    a_lds[i] = row * C::kRow + kv * 8;
+    a_k[i] = kv * 8;
   }
-  u32x4 ga[4], gb[4];
+#pragma unroll
+  for (int i = 0; i < C::kVecB; ++i) {
+    const int v = tid + kThreads * i;
+    const int row = v / C::kKv, kv = v % C::kKv;
+    b_off[i] = static_cast<uint32_t>(row * s.ldw * 2);
+    b_lds[i] = C::kStageA + row * C::kRow + kv * 8;
+    b_k[i] = kv * 8;
+  }
+  u32x4 ga[C::kVecA], gb[C::kVecB];
   auto load_stage = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool in_k = k0 + kv8[i] < p.hidden;
-      const uint32_t ko = static_cast<uint32_t>((k0 + kv8[i]) * 2);
-      ga[i] = ld16(ra, in_k ? a_row_off[i] + ko : a_bytes);
-      gb[i] = ld16(rb, in_k ? b_row_off[i] + ko : b_bytes);
+    for (int i = 0; i < C::kVecA; ++i) {
+      const int k = k0 + a_k[i];
+      ga[i] = ld16(ra, k < p.hidden ? a_off[i] + static_cast<uint32_t>(k * 2) : a_bytes);
+    }
+#pragma unroll
+    for (int i = 0; i < C::kVecB; ++i) {
+      const int k = k0 + b_k[i];
+      gb[i] = ld16(rb, k < p.hidden ? b_off[i] + static_cast<uint32_t>(k * 2) : b_bytes);
     }
   };
   auto store_stage = [&](int buf) {
-    uint16_t* a = lds + buf * 2 * kStage;
-    uint16_t* b = a + kStage;
+    uint16_t* base = lds + buf * C::kStage;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<u32x4*>(a + lds_off[i]) = ga[i];
-      *reinterpret_cast<u32x4*>(b + lds_off[i]) = gb[i];
-    }
+    for (int i = 0; i < C::kVecA; ++i) *reinterpret_cast<u32x4*>(base + a_lds[i]) = ga[i];
+#pragma unroll
+    for (int i = 0; i < C::kVecB; ++i) *reinterpret_cast<u32x4*>(base + b_lds[i]) = gb[i];
   };
+
+  f32x16 acc[WMB][WNB];
+#pragma unroll
+  for (int i = 0; i < WMB; ++i)
+#pragma unroll
+    for (int j = 0; j < WNB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = (p.hidden + BK - 1) / BK;
+  load_stage(0);
+  store_stage(0);
+  __syncthreads();
+  const int frag_row = lane & 31;
+  const int frag_k = (lane >> 5) * 8;
+  const int a_row0 = wm * 32 * WMB + frag_row;
+  const int b_row0 = wn * 32 * WNB + frag_row;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) load_stage((kt + 1) * BK);
+    const uint16_t* a = lds + cur * C::kStage;
+    const uint16_t* b = a + C::kStageA;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      bf16x8 af[WMB], bfr[WNB];
+#pragma unroll
+      for (int i = 0; i < WMB; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(a + (a_row0 + i * 32) * C::kRow + kk + frag_k);
+#pragma unroll
+      for (int j = 0; j < WNB; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8*>(b + (b_row0 + j * 32) * C::kRow + kk + frag_k);
+#pragma unroll
+      for (int i = 0; i < WMB; ++i)
+#pragma unroll
+        for (int j = 0; j < WNB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) store_stage(cur ^ 1);
+    __syncthreads();
+  }
+  epilogue<WMB, WNB, C::kOutRow>(p, s, acc, lds, m0, n0, rows_a, rows_b);
+}
+
+// Direct-to-LDS variant: each stage's operand tiles go from global memory
+// straight into LDS (buffer_load ... lds: lane l's 16 bytes land at the
+// instruction's LDS base + 16 l), through a ring of S stages, so the loads of
+// stage kt + S - 1 are in flight while stage kt is computed and no VGPRs stage
+// the data. Rows are not padded; instead the 16-byte k-slot of each row is
+// XOR-swizzled, slot' = slot ^ ((row / (16 / P)) mod P) with P = BK / 8 slots
+// per row, which puts the 16 rows read by a 16-lane group at 16 distinct
+// 16-byte bank groups. Lane l of a load instruction therefore fetches the
+// global k-vector that belongs at its fixed LDS slot.
+template <int BK, int S>
+struct DlCfg {
+  static constexpr int BM = 128, BN = 128;
+  static constexpr int P = BK / 8;                     // 16-byte slots per row
+  static constexpr int kRowsPerGroup = 16 / P;         // rows sharing a swizzle value
+  static constexpr int kRowBytes = BK * 2;
+  static constexpr int kTileBytes = BM * kRowBytes;    // one operand tile (BM == BN)
+  static constexpr int kStageBytes = 2 * kTileBytes;   // A then B
+  static constexpr int kOutRow = BN + 8;
+  static constexpr int kLdsBytes =
+      (S * kStageBytes > BM * kOutRow * 2) ? S * kStageBytes : BM * kOutRow * 2;
+  static constexpr int kLoadsPerTile = kTileBytes / 1024;      // 1 KB per wave instruction
+  static constexpr int kLoadsPerWave = kLoadsPerTile / 4;      // per operand tile
+  static constexpr int kRowsPerLoad = 1024 / kRowBytes;
+  static_assert(kLoadsPerTile % 4 == 0, "whole load instructions per wavefront");
+  static_assert(kLdsBytes <= 160 * 1024, "LDS");
+};
+
+typedef __attribute__((address_space(3))) unsigned char LdsByte;
+
+// Lane l's 16 bytes at byte offset `voff` of the buffer go to dst + 16 l (LDS).
+// (Called through this helper: with the builtin written directly in a kernel
+// body, the host compilation pass emitted no launch stub for the kernel.)
+__device__ __forceinline__ void load16_to_lds(Rsrc r, LdsByte* dst, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, 0, 0, 0);
+}
+
+__device__ __forceinline__ void vm_wait(int n) {
+  // s_waitcnt vmcnt(n) with lgkmcnt and expcnt left alone (gfx9 encoding)
+  switch (n) {
+    case 4: __builtin_amdgcn_s_waitcnt(0x0F70 | 4); break;
+    case 8: __builtin_amdgcn_s_waitcnt(0x0F70 | 8); break;
+    case 12: __builtin_amdgcn_s_waitcnt(0x0F70 | 12); break;
+    default: __builtin_amdgcn_s_waitcnt(0x0F70 | 0); break;  // 0, and any count not listed
+  }
+}
+
+template <int BK, int S>
+__global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p) {
+  using C = DlCfg<BK, S>;
+  __shared__ __align__(1024) unsigned char lds[C::kLdsBytes];
+  int mt, nt;
+  if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p, mt, nt)) return;
+  const int si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
+  const ProjSegDev& s = p.seg[si];
+  const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
+  const int n0 = (nt - s.tile0) * C::BN;
+  const int rows_a = static_cast<int>((p.T - m0 < C::BM) ? p.T - m0 : C::BM);
+  const int rows_b = (s.d - n0 < C::BN) ? s.d - n0 : C::BN;
+
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const uint32_t a_bytes = static_cast<uint32_t>(rows_a * p.ldx * 2);
+  const uint32_t b_bytes = static_cast<uint32_t>(rows_b * s.ldw * 2);
+  const Rsrc ra = make_rsrc(p.x + m0 * p.ldx, a_bytes);
+  const Rsrc rb = make_rsrc(s.w + static_cast<int64_t>(n0) * s.ldw, b_bytes);
+
+  // this lane's global row offset and k-vector for each of the wave's loads
+  uint32_t a_row[C::kLoadsPerWave], b_row[C::kLoadsPerWave];
+  int kvec[C::kLoadsPerWave];
+#pragma unroll
+  for (int i = 0; i < C::kLoadsPerWave; ++i) {
+    const int row = (wave * C::kLoadsPerWave + i) * C::kRowsPerLoad + lane / C::P;
+    const int slot = lane % C::P;
+    kvec[i] = (slot ^ ((row / C::kRowsPerGroup) % C::P)) * 8;
+    a_row[i] = static_cast<uint32_t>(row * p.ldx * 2);
+    b_row[i] = static_cast<uint32_t>(row * s.ldw * 2);
+  }
+  // Stage `stage` (k from k0) into its ring slot.
+#define QKN_ISSUE_STAGE(stage, k0)                                                          \
+  do {                                                                                      \
+    const int base_ = ((stage) % S) * C::kStageBytes;                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < C::kLoadsPerWave; ++i_) {                       \
+      const int k_ = (k0) + kvec[i_];                                                       \
+      const int slice_ = base_ + (wave * C::kLoadsPerWave + i_) * 1024;                     \
+      load16_to_lds(ra, (LdsByte*)(lds + slice_),                                           \
+                    k_ < p.hidden ? a_row[i_] + static_cast<uint32_t>(k_ * 2) : a_bytes);    \
+      load16_to_lds(rb, (LdsByte*)(lds + C::kTileBytes + slice_),                           \
+                    k_ < p.hidden ? b_row[i_] + static_cast<uint32_t>(k_ * 2) : b_bytes);    \
+    }                                                                                       \
+  } while (0)
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -190,27 +435,38 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = (p.hidden + kBK - 1) / kBK;
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-  const int frag_row = lane & 31;
-  const int frag_k = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) load_stage((kt + 1) * kBK);
-    const uint16_t* a = lds + cur * 2 * kStage;
-    const uint16_t* b = a + kStage;
+  const int nk = (p.hidden + BK - 1) / BK;
 #pragma unroll
-    for (int kk = 0; kk < kBK; kk += 16) {
+  for (int st = 0; st < S - 1; ++st)
+    if (st < nk) QKN_ISSUE_STAGE(st, st * BK);
+
+  const int frag_row = lane & 31;
+  const int frag_kv = lane >> 5;
+  constexpr int kPerStage = 2 * C::kLoadsPerWave;  // load instructions per wave per stage
+  for (int kt = 0; kt < nk; ++kt) {
+    // stages kt + 1 .. kt + S - 2 may stay in flight
+    const int later = (nk - 1 - kt < S - 2) ? nk - 1 - kt : S - 2;
+    vm_wait(later * kPerStage);
+    // A plain barrier, not __syncthreads(): its fence would wait for every
+    // load in flight, the later stages' too. Each wavefront has waited for its
+    // own part of stage kt (the DMA count drops once the data is in LDS), and
+    // its reads of stage kt - 1 were consumed by MFMAs before it got here.
+    __builtin_amdgcn_s_barrier();
+    if (kt + S - 1 < nk) QKN_ISSUE_STAGE(kt + S - 1, (kt + S - 1) * BK);
+    const unsigned char* a = lds + (kt % S) * C::kStageBytes;
+    const unsigned char* b = a + C::kTileBytes;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      const int kv = kk / 8 + frag_kv;
       bf16x8 af[2], bfr[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
+        const int ra_row = wm * 64 + i * 32 + frag_row;
+        const int rb_row = wn * 64 + i * 32 + frag_row;
         af[i] = *reinterpret_cast<const bf16x8*>(
-            a + (wm * 64 + i * 32 + frag_row) * kLdsRow + kk + frag_k);
+            a + ra_row * C::kRowBytes + ((kv ^ ((ra_row / C::kRowsPerGroup) % C::P)) * 16));
         bfr[i] = *reinterpret_cast<const bf16x8*>(
-            b + (wn * 64 + i * 32 + frag_row) * kLdsRow + kk + frag_k);
+            b + rb_row * C::kRowBytes + ((kv ^ ((rb_row / C::kRowsPerGroup) % C::P)) * 16));
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -218,93 +474,81 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (more) store_stage(cur ^ 1);
-    __syncthreads();
   }
-
-  // ---- epilogue: round once to bf16, stage the tile in LDS
-  uint16_t* out = lds;  // [kBM][kOutRow]
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = wn * 64 + j * 32 + (lane & 31);
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const uint32_t pk = pack_bf16x2(acc[i][j][r], acc[i][j][r + 1]);
-        out[row * kOutRow + col] = static_cast<uint16_t>(pk & 0xffffu);
-        out[(row + 1) * kOutRow + col] = static_cast<uint16_t>(pk >> 16);
-      }
-    }
   __syncthreads();
-
-  // coalesced 16-byte stores of the tile rows (columns past d_local skipped)
-  const uint32_t y_bytes = static_cast<uint32_t>(rows_a * s.ldy * 2);
-  const Rsrc ry = make_rsrc(s.y + m0 * s.ldy + n0, y_bytes);
-#pragma unroll
-  for (int i = 0; i < (kBM * kBN / 8) / kThreads; ++i) {
-    const int v = tid + kThreads * i;
-    const int row = v >> 4, cv = (v & 15) * 8;
-    const u32x4 val = *reinterpret_cast<const u32x4*>(out + row * kOutRow + cv);
-    const bool ok = cv < rows_b;  // rows_b = valid columns of this tile
-    st16(val, ry, ok ? static_cast<uint32_t>((row * s.ldy + cv) * 2) : y_bytes);
-  }
-
-  // Phase A over the tile's columns: thread pair (2r, 2r+1) takes row r,
-  // columns [0, 64) and [64, 128) in ascending order; the pair then adds.
-  {
-    const int row = tid >> 1, half = tid & 1;
-    const uint16_t* src = out + row * kOutRow + half * 64;
-    float acc_s = 0.0f;
-#pragma unroll
-    for (int c = 0; c < 64; c += 8) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(src + c);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float lo = bf16_lo(v[e]), hi = bf16_hi(v[e]);
-        acc_s = __builtin_fmaf(lo, lo, acc_s);
-        acc_s = __builtin_fmaf(hi, hi, acc_s);
-      }
-    }
-    // the partner lane's sum (quad_perm [1,0,3,2]: lanes 2r and 2r+1 swap)
-    const float other = __builtin_bit_cast(
-        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc_s), 0xB1, 0xF, 0xF, false));
-    const float first = half ? other : acc_s;
-    const float second = half ? acc_s : other;
-    const float tile_sum = first + second;
-    if (half == 0 && row < rows_a)
-      s.tile_partials[static_cast<int64_t>(nt - s.tile0) * p.T + m0 + row] = tile_sum;
-  }
+  epilogue<2, 2, C::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds), m0, n0, rows_a, rows_b);
+#undef QKN_ISSUE_STAGE
 }
 
-// partials[t] = tile statistics of token t added in ascending tile order.
+// partials[t] = chunk statistics of token t added in ascending chunk order.
 __global__ __launch_bounds__(256) void qkn_proj_finish(const ProjParams p) {
   const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int si = static_cast<int>(blockIdx.y);
   if (t >= p.T || si >= p.nseg) return;
   const ProjSegDev& s = p.seg[si];
   float S = s.tile_partials[t];
-  for (int n = 1; n < s.ntiles; ++n) S = S + s.tile_partials[static_cast<int64_t>(n) * p.T + t];
+  for (int n = 1; n < s.nchunks; ++n) S = S + s.tile_partials[static_cast<int64_t>(n) * p.T + t];
   s.partials[t] = S;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int64_t tiles_of(int64_t d) { return (d + kBN - 1) / kBN; }
+int64_t chunks_of(int64_t d) { return (d + kChunkN - 1) / kChunkN; }
+
+typedef void (*GemmFn)(ProjParams);
+
+// Tile shapes: (rows, columns, k per stage) of a workgroup's tile.
+struct TileShape {
+  GemmFn fn;
+  int bm, bn, bk;
+  int lds_bytes;
+  const char* name;
+};
+#define QKN_TILE(WM, WN, BK, NAME)                                                        \
+  TileShape {                                                                             \
+    qkn_proj_gemm<WM, WN, BK>, 64 * WM, 64 * WN, BK,                                     \
+        static_cast<int>(TileCfg<WM, WN, BK>::kLds * sizeof(uint16_t)), NAME              \
+  }
+#define QKN_DL(BK, S, NAME) \
+  TileShape { qkn_proj_gemm_dl<BK, S>, 128, 128, BK, DlCfg<BK, S>::kLdsBytes, NAME }
+// [0] is the default (measured fastest on MI355X: 128 x 128 tiles, k 64 per
+// stage, two LDS stages filled directly from global memory, two workgroups
+// per CU); [1] is the register-staged kernel.
+const TileShape kTiles[] = {QKN_DL(64, 2, "proj<128x128,64,dl2>"),
+                            QKN_TILE(2, 2, 64, "proj<128x128,64,reg>")};
+constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
+
+// Process-wide choice of tile shape (benchmarks): 0 = automatic, i = kTiles[i - 1].
+int g_tile_choice = 0;
+
+const TileShape& choose_tile(int64_t T, const qkn_proj_seg* segs, int nseg) {
+  (void)T;
+  (void)segs;
+  (void)nseg;
+  if (g_tile_choice > 0 && g_tile_choice <= kNumTiles) return kTiles[g_tile_choice - 1];
+  return kTiles[0];
+}
 
 }  // namespace
+
+namespace qkn_host {
+int set_proj_tile(int64_t choice) {
+  if (choice < 0 || choice > kNumTiles) return QKN_EINVAL;
+  g_tile_choice = static_cast<int>(choice);
+  return QKN_OK;
+}
+}  // namespace qkn_host
 
 extern "C" {
 
 int64_t qkn_proj_workspace_bytes(int64_t T, const qkn_proj_seg* segs, int nseg) {
   if (!segs || nseg < 1 || nseg > 2 || T < 0) return QKN_EINVAL;
-  int64_t tiles = 0;
+  int64_t chunks = 0;
   for (int i = 0; i < nseg; ++i) {
     if (segs[i].d_local < 1) return QKN_EINVAL;
-    tiles += tiles_of(segs[i].d_local);
+    chunks += chunks_of(segs[i].d_local);
   }
-  return 4 * T * tiles;
+  return 4 * T * chunks;
 }
 
 int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
@@ -330,7 +574,7 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
     if (!aligned16(s.w) || !aligned16(s.y) || s.ldw % 8 || s.ldy % 8 || s.d_local % 8 ||
-        s.d_local * s.ldw * 2 >= lim || int64_t{kBM} * s.ldy * 2 >= lim)
+        s.d_local * s.ldw * 2 >= lim || int64_t{256} * s.ldy * 2 >= lim)
       return QKN_ENOTSUP;
   }
 
@@ -355,13 +599,14 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     for (int b = a + 1; b < n; ++b)
       if ((out[a] || out[b]) && spans_overlap(items[a], items[b])) return QKN_EOVERLAP;
 
+  const TileShape& ts = choose_tile(T, segs, nseg);
   ProjParams p;
   memset(&p, 0, sizeof(p));
   p.x = x;
   p.ldx = ldx;
   p.T = T;
   p.hidden = static_cast<int32_t>(hidden);
-  p.m_tiles = static_cast<int32_t>((T + kBM - 1) / kBM);
+  p.m_tiles = static_cast<int32_t>((T + ts.bm - 1) / ts.bm);
   p.nseg = nseg;
   float* ws = static_cast<float*>(workspace);
   int32_t tile0 = 0;
@@ -375,24 +620,23 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     d.ldy = s.ldy;
     d.d = static_cast<int32_t>(s.d_local);
     d.tile0 = tile0;
-    d.ntiles = static_cast<int32_t>(tiles_of(s.d_local));
+    d.nchunks = static_cast<int32_t>(chunks_of(s.d_local));
     d.tile_partials = ws;
-    ws += static_cast<int64_t>(d.ntiles) * T;
-    tile0 += d.ntiles;
+    ws += static_cast<int64_t>(d.nchunks) * T;
+    tile0 += static_cast<int32_t>((s.d_local + ts.bn - 1) / ts.bn);
   }
   p.n_tiles = tile0;
   const int64_t tiles = static_cast<int64_t>(p.m_tiles) * p.n_tiles;
   if (tiles > 0x7fffffff - kXcds) return QKN_ENOTSUP;
   const int64_t grid = (tiles + kXcds - 1) / kXcds * kXcds;
-  const qkn_launch_info info{"proj<128,128>/gemm+phase_a", grid, kThreads, grid * (kThreads / 64),
-                             static_cast<int64_t>(4 * kStage * sizeof(uint16_t))};
+  const qkn_launch_info info{ts.name, grid, kThreads, grid * (kThreads / 64), ts.lds_bytes};
   if (qkn_host::validate_only()) {
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, info.lds_bytes});
     return QKN_OK;
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* args[] = {&p};
-  if (hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_gemm), dim3(static_cast<unsigned>(grid)),
+  if (hipLaunchKernel(reinterpret_cast<const void*>(ts.fn), dim3(static_cast<unsigned>(grid)),
                       dim3(kThreads), args, 0, st) != hipSuccess)
     return QKN_EHIP;
   const dim3 fgrid(static_cast<unsigned>((T + 255) / 256), static_cast<unsigned>(nseg));

@@ -539,3 +539,11 @@ def dry_proj_ok(lib, *args):
         return _proj(lib, *args) == 0
     finally:
         assert lib.qkn_set_option(b"validate_only", 0) == 0
+
+
+def test_proj_tile_option(lib):
+    for v in (0, 1, 2):
+        assert lib.qkn_set_option(b"proj_tile", v) == 0
+    assert lib.qkn_set_option(b"proj_tile", 3) == L.QKN_EINVAL
+    assert lib.qkn_set_option(b"proj_tile", -1) == L.QKN_EINVAL
+    assert lib.qkn_set_option(b"proj_tile", 0) == 0
