@@ -34,7 +34,10 @@
  *   - Arithmetic: inputs are widened exactly, all sums and products are fp32
  *     (Sec. IV-C: fp32 accumulation for bf16 and FP8-E4M3 activations), and
  *     the output is rounded once to the input's format (nearest, ties to
- *     even). NaN and infinities propagate by IEEE rules (eps = 0 with an
+ *     even). The factor 1/sqrt(S/d_full + eps) is evaluated as the hardware
+ *     reciprocal square root (within 1 ulp) of fma(S, 1/d_full, eps), with
+ *     1/d_full rounded to fp32 once: within a few fp32 ulps of the exact
+ *     factor. NaN and infinities propagate by IEEE rules (eps = 0 with an
  *     all-zero row gives NaN).
  *   - Determinism: a row's partial sum depends only on d_local and the row's
  *     values (one fixed fp32 summation tree), never on the launch shape or the

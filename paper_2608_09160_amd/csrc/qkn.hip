@@ -79,7 +79,7 @@ struct DevSeg {
   int64_t ldy;
   int32_t d;        // d_local
   int32_t nchunks;  // ceil(d_local / elements per chunk)
-  float d_full;     // divisor of the mean (H_total)
+  float rcp_d_full; // 1 / H_total rounded to fp32 (the mean's divisor)
   int32_t vec;      // 128-bit accesses allowed
 };
 
@@ -242,8 +242,13 @@ __device__ __forceinline__ float combine_slots_any(const float* partials, int64_
   return S;
 }
 
-__device__ __forceinline__ float rms_inverse(float S, float d_full, float eps) {
-  return 1.0f / sqrtf(S / d_full + eps);
+// Phase B factor 1/sqrt(S/H_total + eps): the hardware reciprocal square root
+// (v_rsq_f32, within 1 ulp) of fma(S, 1/H_total, eps) -- three fp32
+// roundings in all, far below one step of the bf16 or FP8 output, and a
+// fraction of the instructions of a correctly rounded divide and square root
+// (which the per-token critical path of a wavefront measurably feels).
+__device__ __forceinline__ float rms_inverse(float S, float rcp_d_full, float eps) {
+  return __builtin_amdgcn_rsqf(__builtin_fmaf(S, rcp_d_full, eps));
 }
 
 __device__ __forceinline__ int64_t wave_index() {
@@ -545,11 +550,11 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
       }
     }
     const float S0 = combine_slots(slots0, own0, p.tp, own_rank);
-    const float inv0 = rms_inverse(S0, s0.d_full, p.eps);
+    const float inv0 = rms_inverse(S0, s0.rcp_d_full, p.eps);
     float inv1 = 0.0f;
     if constexpr (N1 > 0) {
       const float S1 = combine_slots(slots1, own1, p.tp, own_rank);
-      inv1 = rms_inverse(S1, s1.d_full, p.eps);
+      inv1 = rms_inverse(S1, s1.rcp_d_full, p.eps);
     }
 
     // Phase C.
@@ -721,10 +726,10 @@ __global__ __launch_bounds__(256) void qkn_wide(const KParams p) {
     if constexpr (MODE == kPartial) {
       st4f_lane0(own0, make_rsrc_at(s0.partials, t * 4, 4u), lane);
     } else {
-      const float inv0 = rms_inverse(combine_slots(sl0, own0, p.tp, own_rank), s0.d_full, p.eps);
+      const float inv0 = rms_inverse(combine_slots(sl0, own0, p.tp, own_rank), s0.rcp_d_full, p.eps);
       float inv1 = 0.0f;
       if constexpr (N1 > 0)
-        inv1 = rms_inverse(combine_slots(sl1, own1, p.tp, own_rank), s1.d_full, p.eps);
+        inv1 = rms_inverse(combine_slots(sl1, own1, p.tp, own_rank), s1.rcp_d_full, p.eps);
       // Re-derive the fp32 values from the packed rows instead of keeping the
       // unpacked ones alive from Phase A (an empty asm hides x's value; no code).
 #pragma unroll
@@ -803,7 +808,7 @@ __global__ __launch_bounds__(64) void qkn_generic(const KParams p, int32_t stage
         } else {
           S = combine_slots_any(s.partials, p.T, t, lane, p.tp, own, own_rank);
         }
-        const float inv = rms_inverse(S, s.d_full, p.eps);
+        const float inv = rms_inverse(S, s.rcp_d_full, p.eps);
 
         E* yrow = const_cast<E*>(elem_at<F>(s.y, t, s.ldy, 0));
         for (int c = lane; c < s.nchunks; c += kWave) {
@@ -1124,7 +1129,8 @@ DevSeg to_dev(const HSeg& s, int mode, const FormatInfo& fi) {
   d.ldy = (mode == kPartial || mode == kPublish) ? 0 : s.ldy;
   d.d = static_cast<int32_t>(s.d_local);
   d.nchunks = static_cast<int32_t>((s.d_local + fi.per - 1) / fi.per);
-  d.d_full = static_cast<float>((mode == kPartial || mode == kPublish) ? s.d_local : s.d_full);
+  d.rcp_d_full = static_cast<float>(
+      1.0 / static_cast<double>((mode == kPartial || mode == kPublish) ? s.d_local : s.d_full));
   d.vec = seg_vec_ok(s, mode, fi.per) ? 1 : 0;
   return d;
 }
