@@ -431,19 +431,7 @@ __device__ __forceinline__ float wait_slot(const uint64_t* slots, int64_t T, int
   return v;
 }
 
-// First poll of the other ranks' slots of token t, issued with the token's rows:
-// lanes 0..tp-1 (not `rank`) read slot lane*T + t with one 64-bit agent-coherent
-// load each (the same single-copy-atomic access as the relaxed atomic load);
-// other lanes are out of range and read 0, which no epoch matches.
 constexpr int kCoherentCpol = 16;  // sc1: bypass the CU-local cache
-__device__ __forceinline__ uint64_t poll_slots(const uint64_t* slots, int64_t T, int64_t t,
-                                               int lane, int tp, int rank, bool live) {
-  const uint32_t nrec = static_cast<uint32_t>(((tp - 1) * T + 1) * 8);
-  const Rsrc r = make_rsrc_at(slots, t * 8, live ? nrec : 0u);
-  const int off = (lane < tp && lane != rank) ? static_cast<int>(lane * T * 8)
-                                              : static_cast<int>(nrec);
-  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherentCpol));
-}
 
 // The rank a wavefront computes and where that rank's slice sits: the launch's
 // rank with no offsets, or, when one launch runs every rank of a group, rank
@@ -465,33 +453,114 @@ struct TokenRegs {
   uint64_t word1;
 };
 
+// Byte addresses of one token's rows and slots for each segment, moved by a
+// fixed stride per token, so that a token costs a 64-bit add per address
+// instead of a 64-bit multiply (the scalar instructions of the address
+// arithmetic sit on each wavefront's serial per-token path).
+struct Cursor {
+  uintptr_t x[2];    // token t's row of x at the slice's first column
+  uintptr_t y[2];    // the same for y
+  uintptr_t sl[2];   // rank 0's slot of token t (statistics or flagged slots)
+  uintptr_t own[2];  // this rank's slot of token t
+  uintptr_t inv[2];  // token t's factor (inv_rms + inv_row + t)
+};
+
+// Bytes behind each address, fixed per launch (0: nothing there; a descriptor
+// of 0 bytes reads zeros and drops stores).
+struct CursorBytes {
+  uint32_t row[2];   // live row: nchunks * 16
+  uint32_t sl[2];    // slot reads: (tp - 1) T words + 1
+  uint32_t own[2];   // 4 when the own statistic is stored, else 0
+  uint32_t inv[2];   // 4 when inv_rms is stored, else 0
+};
+
+__device__ __forceinline__ void advance(Cursor& c, const Cursor& step) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    c.x[i] += step.x[i];
+    c.y[i] += step.y[i];
+    c.sl[i] += step.sl[i];
+    c.own[i] += step.own[i];
+    c.inv[i] += step.inv[i];
+  }
+}
+
+__device__ __forceinline__ Rsrc rsrc_of(uintptr_t at, uint32_t bytes) {
+  return make_rsrc(reinterpret_cast<const void*>(at), bytes);
+}
+
+// `live` false: an empty descriptor -- every lane reads zeros, nothing is fetched.
+template <int N>
+__device__ __forceinline__ void load_row_at(uintptr_t row, uint32_t bytes, int lane, u32x4 (&x)[N],
+                                            bool live = true) {
+  const Rsrc r = rsrc_of(row, live ? bytes : 0u);
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = ld16_nt(r, (i * kWave + lane) * 16);
+}
+
+// Lanes 0..tp-1 other than `skip` read rank k's statistic of the token (k*T
+// words after rank 0's); other lanes are out of range and read 0.
+__device__ __forceinline__ float load_slots_at(uintptr_t at, uint32_t nrec, int64_t T, int lane,
+                                               int tp, int skip, bool live = true) {
+  const Rsrc r = rsrc_of(at, live ? nrec : 0u);
+  const int off = (lane < tp && lane != skip) ? static_cast<int>(lane * T * 4)
+                                              : static_cast<int>(nrec);
+  return ld4f(r, off);
+}
+
+// First poll of the other ranks' flagged slots of the token, issued with the
+// token's rows: lanes 0..tp-1 (not `rank`) read slot lane*T of the token with
+// one 64-bit agent-coherent load each (the same single-copy-atomic access as
+// the relaxed atomic load); other lanes are out of range and read 0, which no
+// epoch matches.
+__device__ __forceinline__ uint64_t poll_slots_at(uintptr_t at, uint32_t nrec, int64_t T, int lane,
+                                                  int tp, int rank, bool live) {
+  const Rsrc r = rsrc_of(at, live ? nrec : 0u);
+  const int off = (lane < tp && lane != rank) ? static_cast<int>(lane * T * 8)
+                                              : static_cast<int>(nrec);
+  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherentCpol));
+}
+
+// Phase C: y = round(z * inv), non-temporal 128-bit stores.
+template <class F, int N>
+__device__ __forceinline__ void store_scaled_at(uintptr_t row, uint32_t bytes, int lane,
+                                                const float (&z)[N][F::kPer], float inv) {
+  const Rsrc r = rsrc_of(row, bytes);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    float o[F::kPer];
+#pragma unroll
+    for (int e = 0; e < F::kPer; ++e) o[e] = z[i][e] * inv;
+    st16_nt(F::pack(o), r, (i * kWave + lane) * 16);
+  }
+}
+
 // `live` false (a pipelined request past the last token): nothing is fetched.
 template <class F, int N0, int N1, int MODE>
-__device__ __forceinline__ void fetch_token(const KParams& p, const WaveSlice& ws, int64_t t,
-                                            int lane, int own_rank,
+__device__ __forceinline__ void fetch_token(const KParams& p, const Cursor& c,
+                                            const CursorBytes& nb, int lane, int own_rank,
                                             TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
                                             bool live = true) {
-  load_row<F, N0>(p.seg[0], ws.col0, t, lane, r.x0, live);
-  if constexpr (N1 > 0) load_row<F, N1>(p.seg[1], ws.col1, t, lane, r.x1, live);
+  load_row_at<N0>(c.x[0], nb.row[0], lane, r.x0, live);
+  if constexpr (N1 > 0) load_row_at<N1>(c.x[1], nb.row[1], lane, r.x1, live);
   r.slots0 = 0.0f;
   r.slots1 = 0.0f;
   if constexpr (MODE == kFused || MODE == kApply) {
     // with tp == 1 (fused) every lane is out of range: nothing is read
-    r.slots0 = load_slots_buf(p.seg[0].partials, p.T, t, lane, p.tp, own_rank, live);
-    if constexpr (N1 > 0)
-      r.slots1 = load_slots_buf(p.seg[1].partials, p.T, t, lane, p.tp, own_rank, live);
+    r.slots0 = load_slots_at(c.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, live);
+    if constexpr (N1 > 0) r.slots1 = load_slots_at(c.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, live);
   }
   if constexpr (MODE == kFusedWait) {
-    r.word0 = poll_slots(p.slots[0], p.T, t, lane, p.tp, own_rank, live);
+    r.word0 = poll_slots_at(c.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, live);
     r.word1 = 0;
-    if constexpr (N1 > 0) r.word1 = poll_slots(p.slots[1], p.T, t, lane, p.tp, own_rank, live);
+    if constexpr (N1 > 0) r.word1 = poll_slots_at(c.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, live);
   }
 }
 
-// Phases A, B and C of token t, whose rows and slots are in `r`.
+// Phases A, B and C of the token at cursor `c`, whose rows and slots are in `r`.
 template <class F, int N0, int N1, int MODE>
-__device__ __forceinline__ void process_token(const KParams& p, const WaveSlice& ws, int64_t t,
-                                              int lane, int own_rank,
+__device__ __forceinline__ void process_token(const KParams& p, const Cursor& c,
+                                              const CursorBytes& nb, int lane, int own_rank,
                                               const f32x4 (&g0)[N0][kGammaVecs<F>],
                                               const f32x4 (&g1)[(N1 > 0 ? N1 : 1)][kGammaVecs<F>],
                                               const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
@@ -509,10 +578,10 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
 
   if constexpr (MODE == kPartial) {
     const float own0 = wave_sum(a0);
-    st4f_lane0(own0, make_rsrc_at(s0.partials, t * 4, 4u), lane);
+    st4f_lane0(own0, rsrc_of(c.own[0], nb.own[0]), lane);
   } else if constexpr (MODE == kPublish) {
     const float own0 = wave_sum(a0);
-    if (lane == 0) publish_slot(p.slots[0] + t, own0, p.epoch);
+    if (lane == 0) publish_slot(reinterpret_cast<uint64_t*>(c.own[0]), own0, p.epoch);
   } else {
     float own0 = 0.0f, own1 = 0.0f;
     if constexpr (MODE == kFused || MODE == kFusedWait) {
@@ -522,9 +591,8 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
     if constexpr (MODE == kFusedWait) {
       // publish this rank's statistics before waiting for the others'
       if (lane == 0) {
-        publish_slot(p.slots[0] + static_cast<int64_t>(ws.rank) * p.T + t, own0, p.epoch);
-        if constexpr (N1 > 0)
-          publish_slot(p.slots[1] + static_cast<int64_t>(ws.rank) * p.T + t, own1, p.epoch);
+        publish_slot(reinterpret_cast<uint64_t*>(c.own[0]), own0, p.epoch);
+        if constexpr (N1 > 0) publish_slot(reinterpret_cast<uint64_t*>(c.own[1]), own1, p.epoch);
       }
     }
 
@@ -538,11 +606,11 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
     float slots0 = r.slots0, slots1 = r.slots1;
     if constexpr (MODE == kFusedWait) {
       bool gave_up = false;
-      slots0 = wait_slot(p.slots[0], p.T, t, lane, p.tp, ws.rank, p.epoch, p.spin_limit, given_up,
-                         r.word0, gave_up);
+      slots0 = wait_slot(reinterpret_cast<const uint64_t*>(c.sl[0]), p.T, 0, lane, p.tp, own_rank,
+                         p.epoch, p.spin_limit, given_up, r.word0, gave_up);
       if constexpr (N1 > 0)
-        slots1 = wait_slot(p.slots[1], p.T, t, lane, p.tp, ws.rank, p.epoch, p.spin_limit,
-                           given_up || gave_up, r.word1, gave_up);
+        slots1 = wait_slot(reinterpret_cast<const uint64_t*>(c.sl[1]), p.T, 0, lane, p.tp, own_rank,
+                           p.epoch, p.spin_limit, given_up || gave_up, r.word1, gave_up);
       if (__ballot(gave_up) != 0) {
         if (!given_up && lane == 0)
           __hip_atomic_store(p.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -558,15 +626,55 @@ __device__ __forceinline__ void process_token(const KParams& p, const WaveSlice&
     }
 
     // Phase C.
-    store_scaled<F, N0>(s0, ws.col0, t, lane, z0, inv0);
-    if constexpr (N1 > 0) store_scaled<F, N1>(s1, ws.col1, t, lane, z1, inv1);
-    const int64_t own_slot = (static_cast<int64_t>(ws.rank) * p.T + t) * 4;
+    store_scaled_at<F, N0>(c.y[0], nb.row[0], lane, z0, inv0);
+    if constexpr (N1 > 0) store_scaled_at<F, N1>(c.y[1], nb.row[1], lane, z1, inv1);
     if constexpr (MODE == kFused) {
-      st4f_lane0(own0, make_rsrc_at(s0.partials, own_slot, 4u), lane);
-      if constexpr (N1 > 0) st4f_lane0(own1, make_rsrc_at(s1.partials, own_slot, 4u), lane);
+      st4f_lane0(own0, rsrc_of(c.own[0], nb.own[0]), lane);
+      if constexpr (N1 > 0) st4f_lane0(own1, rsrc_of(c.own[1], nb.own[1]), lane);
     }
-    st4f_lane0(inv0, make_rsrc_at(s0.inv_rms, (ws.inv_row + t) * 4, 4u), lane);
-    if constexpr (N1 > 0) st4f_lane0(inv1, make_rsrc_at(s1.inv_rms, (ws.inv_row + t) * 4, 4u), lane);
+    st4f_lane0(inv0, rsrc_of(c.inv[0], nb.inv[0]), lane);
+    if constexpr (N1 > 0) st4f_lane0(inv1, rsrc_of(c.inv[1], nb.inv[1]), lane);
+  }
+}
+
+// The cursors of token t and their per-token strides (`step` tokens apart).
+template <class F, int MODE>
+__device__ __forceinline__ void make_cursors(const KParams& p, const WaveSlice& ws, int64_t t,
+                                             int64_t step, Cursor& c, Cursor& dc,
+                                             CursorBytes& nb) {
+  constexpr int64_t kEsz = sizeof(typename F::Elem);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const DevSeg& s = p.seg[i];
+    const int64_t col = i == 0 ? ws.col0 : ws.col1;
+    const bool used = i < p.nseg;
+    c.x[i] = reinterpret_cast<uintptr_t>(s.x) + (t * s.ldx + col) * kEsz;
+    dc.x[i] = step * s.ldx * kEsz;
+    c.y[i] = reinterpret_cast<uintptr_t>(s.y) + (t * s.ldy + col) * kEsz;
+    dc.y[i] = step * s.ldy * kEsz;
+    nb.row[i] = used ? static_cast<uint32_t>(s.nchunks) * 16u : 0u;
+    const int64_t own_tok = static_cast<int64_t>(ws.rank) * p.T + t;
+    if constexpr (MODE == kFusedWait || MODE == kPublish) {
+      const uintptr_t base = reinterpret_cast<uintptr_t>(p.slots[i]);
+      c.sl[i] = base + t * 8;
+      c.own[i] = base + ((MODE == kPublish) ? t : own_tok) * 8;
+      dc.sl[i] = dc.own[i] = step * 8;
+      nb.sl[i] = static_cast<uint32_t>(((p.tp - 1) * p.T + 1) * 8);
+      nb.own[i] = 8;
+    } else {
+      const uintptr_t base = reinterpret_cast<uintptr_t>(s.partials);
+      const bool has = base != 0 && used;
+      c.sl[i] = has ? base + t * 4 : 0;
+      c.own[i] = has ? base + ((MODE == kPartial) ? t : own_tok) * 4 : 0;
+      dc.sl[i] = dc.own[i] = has ? step * 4 : 0;
+      nb.sl[i] = has ? static_cast<uint32_t>((p.tp - 1) * p.T * 4 + 4) : 0u;
+      nb.own[i] = has ? 4u : 0u;
+    }
+    const uintptr_t ib = reinterpret_cast<uintptr_t>(s.inv_rms);
+    const bool has_inv = ib != 0 && used;
+    c.inv[i] = has_inv ? ib + (ws.inv_row + t) * 4 : 0;
+    dc.inv[i] = has_inv ? step * 4 : 0;
+    nb.inv[i] = has_inv ? 4u : 0u;
   }
 }
 
@@ -617,29 +725,38 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
     if constexpr (N1 > 0) load_gamma<F, N1>(p.seg[1], ws.col1, lane, g1);
   }
 
+  Cursor c, dc;
+  CursorBytes nb;
+  make_cursors<F, MODE>(p, ws, t, step, c, dc, nb);
   TokenRegs<N0, M1> ra;
-  fetch_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
+  fetch_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, ra);
   if constexpr (PF) {
     TokenRegs<N0, M1> rb;
     const int64_t last = end - 1;
+    Cursor cn = c;
     while (true) {
+      advance(cn, dc);  // token t + step (its requests go nowhere past the last token)
       int64_t tn = t + step;
-      fetch_token<F, N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, rb, tn <= last);
-      process_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
+      fetch_token<F, N0, N1, MODE>(p, cn, nb, lane, own_rank, rb, tn <= last);
+      process_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, g0, g1, ra, given_up);
       if (tn > last) break;
       t = tn;
+      c = cn;
+      advance(cn, dc);
       tn = t + step;
-      fetch_token<F, N0, N1, MODE>(p, ws, tn <= last ? tn : last, lane, own_rank, ra, tn <= last);
-      process_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, rb, given_up);
+      fetch_token<F, N0, N1, MODE>(p, cn, nb, lane, own_rank, ra, tn <= last);
+      process_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, g0, g1, rb, given_up);
       if (tn > last) break;
       t = tn;
+      c = cn;
     }
   } else {
     while (true) {
-      process_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, g0, g1, ra, given_up);
+      process_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, g0, g1, ra, given_up);
       t += step;
       if (t >= end) break;
-      fetch_token<F, N0, N1, MODE>(p, ws, t, lane, own_rank, ra);
+      advance(c, dc);
+      fetch_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, ra);
     }
   }
 }
