@@ -284,9 +284,10 @@ int qkn_last_launch(qkn_launch_info* info);
  *   "waves_per_block" 1..4, 0 = automatic (register path: 1 for bf16,
  *                    4 for fp8; wide path: always 4);
  *   "force_generic"  1 = always take the general path (same results);
- *   "proj_tile"      qkn_proj_partial's kernel: 0 = automatic, 1 = direct-to-
- *                    LDS two-stage kernel (the default), 2 = register-staged
- *                    kernel (same results);
+ *   "proj_tile"      qkn_proj_partial's kernel: 0 = automatic (split k for
+ *                    decode-sized launches, else kernel 1), 1 = direct-to-
+ *                    LDS two-stage kernel, never split, 2 = register-staged
+ *                    kernel, never split (same results as 1);
  *   "validate_only"  1 = entry points validate their arguments and choose a
  *                    kernel (reported by qkn_last_launch, grid 0) but make no
  *                    HIP call and launch nothing.

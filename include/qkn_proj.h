@@ -27,6 +27,15 @@
  * Results are deterministic and independent of the launch shape; they are
  * not bit-identical to qkn_partial_sumsq of y, whose tree differs (both are
  * fp32 sums of the same squares).
+ *
+ * Decode-sized launches (T <= 1024, hidden >= 256) split k into slices (a power
+ * of two, each at least 128 deep and a multiple of 64; at most 16 / ceil(T /
+ * 128) of them) computed by separate workgroups. Each slice's fp32 sum is
+ * stored; a reduction adds the slices in ascending order, rounds once to bf16
+ * and takes the statistic with the same tree as above. The slice count
+ * depends only on T and hidden, so results are deterministic and Q and K in
+ * one launch equal Q and K in two; y's last bit can differ from an unsplit
+ * accumulation (fp32 sums in another order).
  */
 #ifndef QKN_PROJ_H
 #define QKN_PROJ_H
@@ -57,18 +66,22 @@ typedef struct qkn_proj_seg {
 } qkn_proj_seg;
 
 /*
- * Bytes of device workspace qkn_proj_partial needs for these segments and T
- * tokens (the per-tile statistics before they are added in tile order):
- * 4 * T * sum over segments of ceil(d_local / 128). Returns a negative status
- * for invalid arguments (segs NULL, nseg not 1 or 2, T < 0, d_local < 1).
+ * Bytes of device workspace qkn_proj_partial needs for these segments, T
+ * tokens and `hidden` input columns: the per-chunk statistics before they are
+ * added in chunk order (4 * T * sum over segments of ceil(d_local / 128)),
+ * plus, on the split-k path, the per-slice fp32 sums (4 * splits * T * sum
+ * of d_local). Returns a negative status for invalid arguments (segs NULL,
+ * nseg not 1 or 2, T < 0, hidden < 1,
+ * d_local < 1).
  */
-int64_t qkn_proj_workspace_bytes(int64_t T, const qkn_proj_seg* segs, int nseg);
+int64_t qkn_proj_workspace_bytes(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg);
 
 /*
  * Projection of the layer input x (bf16 [T, ldx], columns [0, hidden)) onto
  * 1 or 2 weight slices (Q and K of the same tokens) in one launch, each
  * output tile's Phase A statistic taken in the epilogue, then the tile
- * statistics added in a second, small launch.
+ * statistics added in a second, small launch (split-k: the products, a
+ * reduction, then that small launch).
  *   workspace  device memory of at least qkn_proj_workspace_bytes(...) bytes,
  *              16-byte aligned; its contents on entry do not matter.
  * Requirements of the MFMA path (else QKN_ENOTSUP): x, every w and y 16-byte

@@ -84,7 +84,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qkn_apply_fp8.argtypes = lib.qkn_apply.argtypes
     lib.qkn_fused_shard_fp8.argtypes = lib.qkn_fused_shard.argtypes
     lib.qkn_full_fp8.argtypes = lib.qkn_full.argtypes
-    lib.qkn_proj_workspace_bytes.argtypes = [_c_i64, ctypes.POINTER(QknProjSeg), ctypes.c_int]
+    lib.qkn_proj_workspace_bytes.argtypes = [_c_i64, _c_i64, ctypes.POINTER(QknProjSeg), ctypes.c_int]
     lib.qkn_proj_workspace_bytes.restype = _c_i64
     lib.qkn_proj_partial.argtypes = [_vp, _c_i64, _c_i64, _c_i64, ctypes.POINTER(QknProjSeg),
                                      ctypes.c_int, _vp, _c_i64, _vp]
@@ -393,11 +393,11 @@ def _proj_segs(segs: Sequence[ProjSeg], T: int, hidden: int, device):
     return arr
 
 
-def qkn_proj_workspace_bytes(T: int, segs: Sequence[ProjSeg]) -> int:
+def qkn_proj_workspace_bytes(T: int, hidden: int, segs: Sequence[ProjSeg]) -> int:
     arr = (QknProjSeg * len(segs))()
     for i, s in enumerate(segs):
         arr[i] = QknProjSeg(None, 0, None, 0, None, s.w.shape[0])
-    n = load().qkn_proj_workspace_bytes(T, arr, len(segs))
+    n = load().qkn_proj_workspace_bytes(T, hidden, arr, len(segs))
     if n < 0:
         raise QknError(int(n), "qkn_proj_workspace_bytes")
     return int(n)
@@ -413,7 +413,7 @@ def qkn_proj_partial(x: torch.Tensor, segs: Sequence[ProjSeg],
     """
     px, ldx, T, hidden = _rows(x, "x")
     arr = _proj_segs(segs, T, hidden, x.device)
-    need = qkn_proj_workspace_bytes(T, segs)
+    need = qkn_proj_workspace_bytes(T, hidden, segs)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
     if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
@@ -430,7 +430,7 @@ class PreparedProj:
         self.x, self.segs = x, list(segs)
         self._px, self._ldx, self._T, self._hidden = _rows(x, "x")
         self._arr = _proj_segs(self.segs, self._T, self._hidden, x.device)
-        need = qkn_proj_workspace_bytes(self._T, self.segs)
+        need = qkn_proj_workspace_bytes(self._T, self._hidden, self.segs)
         self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
         self._lib = load()
 

@@ -77,6 +77,7 @@ struct ProjSegDev {
   int32_t d;
   int32_t tile0;         // first column tile of this segment in the launch
   int32_t nchunks;       // ceil(d / 128)
+  int32_t col0;          // split-k: first column of this segment in the partial sums
 };
 
 struct ProjParams {
@@ -88,6 +89,13 @@ struct ProjParams {
   int32_t n_tiles;       // column tiles of all segments
   int32_t nseg;
   ProjSegDev seg[2];
+  // split-k (few tiles): k-slice s of every tile adds its fp32 products into
+  // part[s][t][c], c over the columns of both segments (segment i's first
+  // column at seg[i].col0)
+  int32_t splits;        // 1: no split
+  int32_t kslice;        // k per slice, a multiple of the stage k
+  float* part;
+  int32_t ncols;         // columns of both segments
 };
 
 __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
@@ -114,11 +122,9 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) {
   return __builtin_bit_cast(float, u & 0xffff0000u);
 }
 
-// Tile number -> (row tile, column tile): XCD-contiguous runs, then groups of
-// kGroupM row tiles sweeping all column tiles.
-__device__ __forceinline__ bool tile_of(int bid, int grid, const ProjParams& p, int& mt, int& nt) {
-  const int per_xcd = grid / kXcds;  // the grid is a multiple of kXcds
-  const int logical = (bid % kXcds) * per_xcd + bid / kXcds;
+// Tile in the grouped order -> (row tile, column tile): groups of kGroupM row
+// tiles, each sweeping all column tiles.
+__device__ __forceinline__ bool tile_from(int logical, const ProjParams& p, int& mt, int& nt) {
   if (logical >= p.m_tiles * p.n_tiles) return false;
   const int group_size = kGroupM * p.n_tiles;
   const int group = logical / group_size;
@@ -128,6 +134,14 @@ __device__ __forceinline__ bool tile_of(int bid, int grid, const ProjParams& p, 
   mt = first_m + in_group % gm;
   nt = in_group / gm;
   return true;
+}
+
+// Tile number -> (row tile, column tile): XCD-contiguous runs, then groups of
+// kGroupM row tiles sweeping all column tiles.
+__device__ __forceinline__ bool tile_of(int bid, int grid, const ProjParams& p, int& mt, int& nt) {
+  const int per_xcd = grid / kXcds;  // the grid is a multiple of kXcds
+  const int logical = (bid % kXcds) * per_xcd + bid / kXcds;
+  return tile_from(logical, p, mt, nt);
 }
 
 // Epilogue of a (64 WMB) x (64 WNB) tile: round the fp32 accumulators once to
@@ -369,22 +383,37 @@ __device__ __forceinline__ void load16_to_lds(Rsrc r, LdsByte* dst, uint32_t vof
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, 0, 0, 0);
 }
 
+// s_waitcnt vmcnt(n), lgkmcnt and expcnt left alone (gfx9 encoding: vmcnt bits
+// [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8])
+constexpr int vmcnt_imm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
+
 __device__ __forceinline__ void vm_wait(int n) {
-  // s_waitcnt vmcnt(n) with lgkmcnt and expcnt left alone (gfx9 encoding)
   switch (n) {
-    case 4: __builtin_amdgcn_s_waitcnt(0x0F70 | 4); break;
-    case 8: __builtin_amdgcn_s_waitcnt(0x0F70 | 8); break;
-    case 12: __builtin_amdgcn_s_waitcnt(0x0F70 | 12); break;
-    default: __builtin_amdgcn_s_waitcnt(0x0F70 | 0); break;  // 0, and any count not listed
+    case 4: __builtin_amdgcn_s_waitcnt(vmcnt_imm(4)); break;
+    case 8: __builtin_amdgcn_s_waitcnt(vmcnt_imm(8)); break;
+    case 12: __builtin_amdgcn_s_waitcnt(vmcnt_imm(12)); break;
+    case 16: __builtin_amdgcn_s_waitcnt(vmcnt_imm(16)); break;
+    case 24: __builtin_amdgcn_s_waitcnt(vmcnt_imm(24)); break;
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;  // 0, and any count not listed
   }
 }
 
-template <int BK, int S>
+// SPLIT: workgroup b takes k-slice b mod splits of tile b / splits and adds
+// its fp32 products into the partial sums instead of running the epilogue.
+template <int BK, int S, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p) {
   using C = DlCfg<BK, S>;
   __shared__ __align__(1024) unsigned char lds[C::kLdsBytes];
   int mt, nt;
-  if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p, mt, nt)) return;
+  int k_lo = 0, k_hi = p.hidden;
+  if constexpr (SPLIT) {
+    const int b = static_cast<int>(blockIdx.x);
+    if (!tile_from(b / p.splits, p, mt, nt)) return;
+    k_lo = (b % p.splits) * p.kslice;
+    k_hi = (k_lo + p.kslice < p.hidden) ? k_lo + p.kslice : p.hidden;
+  } else {
+    if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p, mt, nt)) return;
+  }
   const int si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
   const ProjSegDev& s = p.seg[si];
   const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
@@ -421,9 +450,9 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
       const int k_ = (k0) + kvec[i_];                                                       \
       const int slice_ = base_ + (wave * C::kLoadsPerWave + i_) * 1024;                     \
       load16_to_lds(ra, (LdsByte*)(lds + slice_),                                           \
-                    k_ < p.hidden ? a_row[i_] + static_cast<uint32_t>(k_ * 2) : a_bytes);    \
+                    k_ < k_hi ? a_row[i_] + static_cast<uint32_t>(k_ * 2) : a_bytes);        \
       load16_to_lds(rb, (LdsByte*)(lds + C::kTileBytes + slice_),                           \
-                    k_ < p.hidden ? b_row[i_] + static_cast<uint32_t>(k_ * 2) : b_bytes);    \
+                    k_ < k_hi ? b_row[i_] + static_cast<uint32_t>(k_ * 2) : b_bytes);        \
     }                                                                                       \
   } while (0)
 
@@ -435,10 +464,10 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = (p.hidden + BK - 1) / BK;
+  const int nk = (k_hi - k_lo + BK - 1) / BK;
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
-    if (st < nk) QKN_ISSUE_STAGE(st, st * BK);
+    if (st < nk) QKN_ISSUE_STAGE(st, k_lo + st * BK);
 
   const int frag_row = lane & 31;
   const int frag_kv = lane >> 5;
@@ -452,7 +481,7 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
     // own part of stage kt (the DMA count drops once the data is in LDS), and
     // its reads of stage kt - 1 were consumed by MFMAs before it got here.
     __builtin_amdgcn_s_barrier();
-    if (kt + S - 1 < nk) QKN_ISSUE_STAGE(kt + S - 1, (kt + S - 1) * BK);
+    if (kt + S - 1 < nk) QKN_ISSUE_STAGE(kt + S - 1, k_lo + (kt + S - 1) * BK);
     const unsigned char* a = lds + (kt % S) * C::kStageBytes;
     const unsigned char* b = a + C::kTileBytes;
 #pragma unroll
@@ -475,9 +504,67 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
   }
-  __syncthreads();
-  epilogue<2, 2, C::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds), m0, n0, rows_a, rows_b);
+  if constexpr (SPLIT) {
+    // fp32 products of this k-slice: lanes 0..31 of a row are 32 adjacent columns
+    float* part = p.part + static_cast<int64_t>(static_cast<int>(blockIdx.x) % p.splits) * p.T * p.ncols;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row < rows_a && col < rows_b)
+            part[(m0 + row) * p.ncols + s.col0 + n0 + col] = acc[i][j][r];
+        }
+      }
+  } else {
+    __syncthreads();
+    epilogue<2, 2, C::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds), m0, n0, rows_a, rows_b);
+  }
 #undef QKN_ISSUE_STAGE
+}
+
+// Split-k reduction, one wavefront per (128-column chunk, token): each lane
+// adds two columns' k-slice products in ascending slice order and rounds them
+// once to bf16 (y); the chunk's statistic then follows the tile epilogue's
+// tree (two ascending FMA chains over the chunk's halves, first + second)
+// into tile_partials, which qkn_proj_finish adds in chunk order.
+__global__ __launch_bounds__(64) void qkn_proj_reduce(const ProjParams p) {
+  __shared__ float vals[kChunkN];
+  const int64_t t = blockIdx.y;
+  const int g = static_cast<int>(blockIdx.x);  // chunk over both segments
+  const int si = (p.nseg == 2 && g >= p.seg[0].nchunks) ? 1 : 0;
+  const ProjSegDev& s = p.seg[si];
+  const int q = g - (si ? p.seg[0].nchunks : 0);
+  const int lane = static_cast<int>(threadIdx.x);
+  const int c = q * kChunkN + 2 * lane;  // d_local is a multiple of 8: c < d means c + 1 < d
+  float v0 = 0.0f, v1 = 0.0f;
+  if (c < s.d) {
+    const int64_t slice = p.T * p.ncols;
+    const float* src = p.part + t * p.ncols + s.col0 + c;
+    f32x2 a = *reinterpret_cast<const f32x2*>(src);
+    for (int k = 1; k < p.splits; ++k) {
+      const f32x2 b = *reinterpret_cast<const f32x2*>(src + k * slice);
+      a[0] = a[0] + b[0];
+      a[1] = a[1] + b[1];
+    }
+    const uint32_t pk = pack_bf16x2(a[0], a[1]);
+    *reinterpret_cast<uint32_t*>(s.y + t * s.ldy + c) = pk;
+    v0 = bf16_lo(pk);
+    v1 = bf16_hi(pk);
+  }
+  vals[2 * lane] = v0;  // columns past d_local hold 0, which adds nothing
+  vals[2 * lane + 1] = v1;
+  __syncthreads();
+  const float* h = vals + (lane & 1) * 64;
+  float acc_s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 64; ++i) acc_s = __builtin_fmaf(h[i], h[i], acc_s);
+  const float other = __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc_s), 0xB1, 0xF, 0xF, false));
+  if (lane == 0) s.tile_partials[static_cast<int64_t>(q) * p.T + t] = acc_s + other;
 }
 
 // partials[t] = chunk statistics of token t added in ascending chunk order.
@@ -510,7 +597,7 @@ struct TileShape {
         static_cast<int>(TileCfg<WM, WN, BK>::kLds * sizeof(uint16_t)), NAME              \
   }
 #define QKN_DL(BK, S, NAME) \
-  TileShape { qkn_proj_gemm_dl<BK, S>, 128, 128, BK, DlCfg<BK, S>::kLdsBytes, NAME }
+  TileShape { qkn_proj_gemm_dl<BK, S, false>, 128, 128, BK, DlCfg<BK, S>::kLdsBytes, NAME }
 // [0] is the default (measured fastest on MI355X: 128 x 128 tiles, k 64 per
 // stage, two LDS stages filled directly from global memory, two workgroups
 // per CU); [1] is the register-staged kernel.
@@ -521,12 +608,53 @@ constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 // Process-wide choice of tile shape (benchmarks): 0 = automatic, i = kTiles[i - 1].
 int g_tile_choice = 0;
 
-const TileShape& choose_tile(int64_t T, const qkn_proj_seg* segs, int nseg) {
-  (void)T;
-  (void)segs;
-  (void)nseg;
+const TileShape& choose_tile() {
   if (g_tile_choice > 0 && g_tile_choice <= kNumTiles) return kTiles[g_tile_choice - 1];
   return kTiles[0];
+}
+
+// Split-k (k-slices of a tile in separate workgroups, added by a reduction)
+// for decode-sized launches, whose row tiles alone would leave most CUs idle:
+// at most kSplitMaxRowTiles row tiles (1024 tokens). The slice count is the
+// largest power of two with (row tiles) x (slices) <= kSplitRowSlices and
+// slices at least 128 deep. It depends on T and hidden only -- not on the
+// columns or the segments -- so Q and K launched together or apart, and any
+// device, give the same bits.
+constexpr int64_t kSplitMaxRowTiles = 8;
+constexpr int64_t kSplitRowSlices = 16;
+constexpr int kSplitBk = 64;
+constexpr int kSplitStages = 4;  // a 256-deep slice has all its loads in flight at once
+
+struct Plan {
+  int64_t m_tiles, n_tiles, chunks, ncols;
+  int splits, kslice;
+  int64_t ws_bytes;
+};
+
+Plan plan_of(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg) {
+  Plan pl{};
+  pl.m_tiles = (T + 127) / 128;
+  for (int i = 0; i < nseg; ++i) {
+    pl.n_tiles += (segs[i].d_local + 127) / 128;
+    pl.chunks += chunks_of(segs[i].d_local);
+    pl.ncols += segs[i].d_local;
+  }
+  pl.splits = 1;
+  pl.kslice = static_cast<int>(hidden);
+  if (g_tile_choice == 0 && pl.m_tiles <= kSplitMaxRowTiles) {
+    int splits = 1;
+    while (pl.m_tiles * splits * 2 <= kSplitRowSlices && hidden >= int64_t{128} * splits * 2)
+      splits *= 2;
+    if (splits > 1) {
+      const int64_t per = (hidden + splits - 1) / splits;
+      pl.kslice = static_cast<int>((per + kSplitBk - 1) / kSplitBk * kSplitBk);
+      pl.splits = static_cast<int>((hidden + pl.kslice - 1) / pl.kslice);
+    }
+  }
+  pl.ws_bytes = 4 * T * pl.chunks;  // chunk statistics
+  if (pl.splits > 1) pl.ws_bytes += 4 * int64_t{pl.splits} * T * pl.ncols;  // slice products
+
+  return pl;
 }
 
 }  // namespace
@@ -541,14 +669,11 @@ int set_proj_tile(int64_t choice) {
 
 extern "C" {
 
-int64_t qkn_proj_workspace_bytes(int64_t T, const qkn_proj_seg* segs, int nseg) {
-  if (!segs || nseg < 1 || nseg > 2 || T < 0) return QKN_EINVAL;
-  int64_t chunks = 0;
-  for (int i = 0; i < nseg; ++i) {
+int64_t qkn_proj_workspace_bytes(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg) {
+  if (!segs || nseg < 1 || nseg > 2 || T < 0 || hidden < 1) return QKN_EINVAL;
+  for (int i = 0; i < nseg; ++i)
     if (segs[i].d_local < 1) return QKN_EINVAL;
-    chunks += chunks_of(segs[i].d_local);
-  }
-  return 4 * T * chunks;
+  return plan_of(T, hidden, segs, nseg).ws_bytes;
 }
 
 int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
@@ -563,7 +688,8 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   if (!x) return QKN_EINVAL;
   for (int i = 0; i < nseg; ++i)
     if (!segs[i].w || !segs[i].y || !segs[i].partials) return QKN_EINVAL;
-  const int64_t need = qkn_proj_workspace_bytes(T, segs, nseg);
+  const Plan pl = plan_of(T, hidden, segs, nseg);
+  const int64_t need = pl.ws_bytes;
   if (!workspace || workspace_bytes < need) return QKN_EINVAL;
 
   // the MFMA path's shape and alignment requirements
@@ -599,7 +725,8 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     for (int b = a + 1; b < n; ++b)
       if ((out[a] || out[b]) && spans_overlap(items[a], items[b])) return QKN_EOVERLAP;
 
-  const TileShape& ts = choose_tile(T, segs, nseg);
+  const TileShape& ts = choose_tile();
+  const bool split = pl.splits > 1;
   ProjParams p;
   memset(&p, 0, sizeof(p));
   p.x = x;
@@ -608,8 +735,13 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   p.hidden = static_cast<int32_t>(hidden);
   p.m_tiles = static_cast<int32_t>((T + ts.bm - 1) / ts.bm);
   p.nseg = nseg;
+  p.splits = pl.splits;
+  p.kslice = pl.kslice;
+  p.ncols = static_cast<int32_t>(pl.ncols);
   float* ws = static_cast<float*>(workspace);
-  int32_t tile0 = 0;
+  p.part = split ? ws : nullptr;
+  if (split) ws += int64_t{pl.splits} * T * pl.ncols;
+  int32_t tile0 = 0, col0 = 0;
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
     ProjSegDev& d = p.seg[i];
@@ -620,28 +752,38 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     d.ldy = s.ldy;
     d.d = static_cast<int32_t>(s.d_local);
     d.tile0 = tile0;
+    d.col0 = col0;
     d.nchunks = static_cast<int32_t>(chunks_of(s.d_local));
     d.tile_partials = ws;
     ws += static_cast<int64_t>(d.nchunks) * T;
     tile0 += static_cast<int32_t>((s.d_local + ts.bn - 1) / ts.bn);
+    col0 += static_cast<int32_t>(s.d_local);
   }
   p.n_tiles = tile0;
   const int64_t tiles = static_cast<int64_t>(p.m_tiles) * p.n_tiles;
-  if (tiles > 0x7fffffff - kXcds) return QKN_ENOTSUP;
-  const int64_t grid = (tiles + kXcds - 1) / kXcds * kXcds;
-  const qkn_launch_info info{ts.name, grid, kThreads, grid * (kThreads / 64), ts.lds_bytes};
+  if (tiles * pl.splits > 0x7fffffff - kXcds) return QKN_ENOTSUP;
+  const int64_t grid = split ? tiles * pl.splits : (tiles + kXcds - 1) / kXcds * kXcds;
+  const char* name = split ? "proj<128x128,64,dl4,splitk>" : ts.name;
+  const int lds = split ? DlCfg<kSplitBk, kSplitStages>::kLdsBytes : ts.lds_bytes;
+  const qkn_launch_info info{name, grid, kThreads, grid * (kThreads / 64), lds};
   if (qkn_host::validate_only()) {
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, info.lds_bytes});
     return QKN_OK;
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* args[] = {&p};
-  if (hipLaunchKernel(reinterpret_cast<const void*>(ts.fn), dim3(static_cast<unsigned>(grid)),
-                      dim3(kThreads), args, 0, st) != hipSuccess)
+  const void* gemm = split ? reinterpret_cast<const void*>(qkn_proj_gemm_dl<kSplitBk, kSplitStages, true>)
+                           : reinterpret_cast<const void*>(ts.fn);
+  if (hipLaunchKernel(gemm, dim3(static_cast<unsigned>(grid)), dim3(kThreads), args, 0, st) !=
+      hipSuccess)
+    return QKN_EHIP;
+  if (split && hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_reduce),
+                               dim3(static_cast<unsigned>(pl.chunks), static_cast<unsigned>(T)),
+                               dim3(64), args, 0, st) != hipSuccess)
     return QKN_EHIP;
   const dim3 fgrid(static_cast<unsigned>((T + 255) / 256), static_cast<unsigned>(nseg));
-  if (hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_finish), fgrid, dim3(256), args, 0, st) !=
-      hipSuccess)
+  if (hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_finish), fgrid, dim3(256), args, 0,
+                      st) != hipSuccess)
     return QKN_EHIP;
   qkn_host::record_launch(info);
   return QKN_OK;

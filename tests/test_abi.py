@@ -492,19 +492,35 @@ def _proj(lib, x, ldx, T, hidden, segs, ws, ws_bytes):
 
 def test_proj_workspace_size(lib):
     segs = (L.QknProjSeg * 2)(_pseg(0, 0, 0, 0, 0, 2048), _pseg(0, 0, 0, 0, 0, 520))
-    assert lib.qkn_proj_workspace_bytes(8192, segs, 2) == 4 * 8192 * (16 + 5)
-    assert lib.qkn_proj_workspace_bytes(8192, segs, 1) == 4 * 8192 * 16
-    assert lib.qkn_proj_workspace_bytes(-1, segs, 1) == L.QKN_EINVAL
-    assert lib.qkn_proj_workspace_bytes(8, segs, 3) == L.QKN_EINVAL
+    # many tiles: per-chunk statistics
+    assert lib.qkn_proj_workspace_bytes(8192, 4096, segs, 2) == 4 * 8192 * (16 + 5)
+    assert lib.qkn_proj_workspace_bytes(8192, 4096, segs, 1) == 4 * 8192 * 16
+    # decode: one row tile -> 16 slices of 256 (row tiles x slices <= 16, slices >= 128
+    # deep): the slices' fp32 products, then the chunk statistics
+    def split_ws(T, splits, ncols, chunks):
+        return 4 * splits * T * ncols + 4 * T * chunks
+    assert lib.qkn_proj_workspace_bytes(64, 4096, segs, 2) == split_ws(64, 16, 2048 + 520, 21)
+    assert lib.qkn_proj_workspace_bytes(64, 4096, segs, 1) == split_ws(64, 16, 2048, 16)
+    # the slice count depends on T and hidden only
+    assert lib.qkn_proj_workspace_bytes(300, 4096, segs, 2) == split_ws(300, 4, 2048 + 520, 21)
+    assert lib.qkn_proj_workspace_bytes(1024, 4096, segs, 2) == split_ws(1024, 2, 2048 + 520, 21)
+    assert lib.qkn_proj_workspace_bytes(1025, 4096, segs, 2) == 4 * 1025 * (16 + 5)
+    # a shallow hidden caps the slices at 128 deep: 384 -> slices of 192 (three 64-wide stages)
+    assert lib.qkn_proj_workspace_bytes(64, 384, segs, 2) == split_ws(64, 2, 2048 + 520, 21)
+    assert lib.qkn_proj_workspace_bytes(64, 200, segs, 2) == 4 * 64 * (16 + 5)
+    assert lib.qkn_proj_workspace_bytes(-1, 4096, segs, 1) == L.QKN_EINVAL
+    assert lib.qkn_proj_workspace_bytes(8, 0, segs, 1) == L.QKN_EINVAL
+    assert lib.qkn_proj_workspace_bytes(8, 4096, segs, 3) == L.QKN_EINVAL
     bad = (L.QknProjSeg * 1)(_pseg(0, 0, 0, 0, 0, 0))
-    assert lib.qkn_proj_workspace_bytes(8, bad, 1) == L.QKN_EINVAL
+    assert lib.qkn_proj_workspace_bytes(8, 4096, bad, 1) == L.QKN_EINVAL
 
 
 def test_proj_validation(lib):
     T, h = 300, 4096
     X, W, Y, P, WS = BASE, BASE + 64 * MB, BASE + 128 * MB, BASE + 192 * MB, BASE + 200 * MB
     ok = _pseg(W, h, Y, 2048, P, 2048)
-    need = 4 * T * 16
+    need = lib.qkn_proj_workspace_bytes(T, h, (L.QknProjSeg * 1)(ok), 1)
+    assert need > 4 * T * 16  # 3 row tiles: the split-k path
     # T == 0 is a no-op even with NULL pointers
     assert _proj(lib, None, h, 0, h, [ok], None, 0) == 0
     assert _proj(lib, X, h, T, h, [ok], WS, need - 4) == L.QKN_EINVAL          # workspace too small
@@ -526,7 +542,7 @@ def test_proj_validation(lib):
     assert _proj(lib, X, h, T, h, [ok], W + 4096, need) == L.QKN_EOVERLAP
     q = _pseg(W, h, Y, 2560, P, 2048)
     k = _pseg(W + 32 * MB, h, Y + 2048 * 2, 2560, P + MB, 512)
-    need2 = 4 * T * (16 + 4)
+    need2 = lib.qkn_proj_workspace_bytes(T, h, (L.QknProjSeg * 2)(q, k), 2)
     assert dry_proj_ok(lib, X, h, T, h, [q, k], WS, need2)
     k_bad = _pseg(W + 32 * MB, h, Y + 2040 * 2, 2560, P + MB, 512)
     assert _proj(lib, X, h, T, h, [q, k_bad], WS, need2) == L.QKN_EOVERLAP

@@ -194,3 +194,33 @@ def test_both_kernels_give_the_same_bits():
         assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
     for (y, part), w, t in zip(outs[0], ws, "qk"):
         _check(x, w, y, part, t)
+
+
+@pytest.mark.parametrize("T,hidden", [(64, 4096), (1, 1096), (1024, 512)])
+def test_split_k_against_one_slice(T, hidden):
+    """Decode-sized launches split k into slices added in ascending order; the
+    forced single-slice kernel sums the same products in another order. Both
+    pass the oracle, so they differ by at most twice the error bound; and as
+    the same fp32 sums in two orders, most stored values are identical."""
+    rng = np.random.default_rng(T + hidden)
+    dq, dk = 1024, 264
+    x = workloads.f32_to_bf16_bits(rng.standard_normal((T, hidden), dtype=np.float32))
+    ws = [workloads.f32_to_bf16_bits(rng.standard_normal((d, hidden), dtype=np.float32) / np.sqrt(hidden))
+          for d in (dq, dk)]
+    print(f"[proj] split k T={T} hidden={hidden}", flush=True)
+    split, info = _run(x, ws)
+    assert info["kernel"].endswith("splitk>"), info
+    L.qkn_set_option("proj_tile", 1)
+    try:
+        whole, info1 = _run(x, ws)
+    finally:
+        L.qkn_set_option("proj_tile", 0)
+    assert not info1["kernel"].endswith("splitk>"), info1
+    for (ys, ps), (yw, pw), w, t in zip(split, whole, ws, "qk"):
+        _check(x, w, ys, ps, f"{t} split")
+        _check(x, w, yw, pw, f"{t} one slice")
+        a, b = Q.decode_bf16(ys), Q.decode_bf16(yw)
+        assert np.mean(a == b) > 0.9, (t, float(np.mean(a == b)))
+    again, _ = _run(x, ws)
+    for a, b in zip(again, split):
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
