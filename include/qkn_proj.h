@@ -28,9 +28,10 @@
  * not bit-identical to qkn_partial_sumsq of y, whose tree differs (both are
  * fp32 sums of the same squares).
  *
- * Decode-sized launches (T <= 1024, hidden >= 256) split k into slices (a power
- * of two, each at least 128 deep and a multiple of 64; at most 16 / ceil(T /
- * 128) of them) computed by separate workgroups. Each slice's fp32 sum is
+ * Decode-sized launches (T <= 1024, hidden >= 256) split k into 2^s contiguous
+ * slices of ceil(hidden / 2^s) rounded up to a multiple of 8 (the last one
+ * shorter), with 2^s the largest power of two <= 16 / ceil(T / 128) that
+ * keeps slices at least 128 deep, computed by separate workgroups. Each slice's fp32 sum is
  * stored; a reduction adds the slices in ascending order, rounds once to bf16
  * and takes the statistic with the same tree as above. The slice count
  * depends only on T and hidden, so results are deterministic and Q and K in
@@ -69,8 +70,8 @@ typedef struct qkn_proj_seg {
  * Bytes of device workspace qkn_proj_partial needs for these segments, T
  * tokens and `hidden` input columns: the per-chunk statistics before they are
  * added in chunk order (4 * T * sum over segments of ceil(d_local / 128)),
- * plus, on the split-k path, the per-slice fp32 sums (4 * splits * T * sum
- * of d_local). Returns a negative status for invalid arguments (segs NULL,
+ * or, on the split-k path, the per-slice fp32 sums (4 * splits * T * sum of
+ * d_local). Returns a negative status for invalid arguments (segs NULL,
  * nseg not 1 or 2, T < 0, hidden < 1,
  * d_local < 1).
  */
@@ -80,8 +81,8 @@ int64_t qkn_proj_workspace_bytes(int64_t T, int64_t hidden, const qkn_proj_seg* 
  * Projection of the layer input x (bf16 [T, ldx], columns [0, hidden)) onto
  * 1 or 2 weight slices (Q and K of the same tokens) in one launch, each
  * output tile's Phase A statistic taken in the epilogue, then the tile
- * statistics added in a second, small launch (split-k: the products, a
- * reduction, then that small launch).
+ * statistics added in a second, small launch (split-k: the slice sums, then
+ * one reduction launch that also adds the statistics).
  *   workspace  device memory of at least qkn_proj_workspace_bytes(...) bytes,
  *              16-byte aligned; its contents on entry do not matter.
  * Requirements of the MFMA path (else QKN_ENOTSUP): x, every w and y 16-byte

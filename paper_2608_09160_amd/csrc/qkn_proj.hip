@@ -526,45 +526,73 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
 #undef QKN_ISSUE_STAGE
 }
 
-// Split-k reduction, one wavefront per (128-column chunk, token): each lane
-// adds two columns' k-slice products in ascending slice order and rounds them
-// once to bf16 (y); the chunk's statistic then follows the tile epilogue's
-// tree (two ascending FMA chains over the chunk's halves, first + second)
-// into tile_partials, which qkn_proj_finish adds in chunk order.
-__global__ __launch_bounds__(64) void qkn_proj_reduce(const ProjParams p) {
-  __shared__ float vals[kChunkN];
-  const int64_t t = blockIdx.y;
-  const int g = static_cast<int>(blockIdx.x);  // chunk over both segments
-  const int si = (p.nseg == 2 && g >= p.seg[0].nchunks) ? 1 : 0;
-  const ProjSegDev& s = p.seg[si];
-  const int q = g - (si ? p.seg[0].nchunks : 0);
-  const int lane = static_cast<int>(threadIdx.x);
-  const int c = q * kChunkN + 2 * lane;  // d_local is a multiple of 8: c < d means c + 1 < d
-  float v0 = 0.0f, v1 = 0.0f;
-  if (c < s.d) {
-    const int64_t slice = p.T * p.ncols;
-    const float* src = p.part + t * p.ncols + s.col0 + c;
-    f32x2 a = *reinterpret_cast<const f32x2*>(src);
-    for (int k = 1; k < p.splits; ++k) {
-      const f32x2 b = *reinterpret_cast<const f32x2*>(src + k * slice);
-      a[0] = a[0] + b[0];
-      a[1] = a[1] + b[1];
-    }
-    const uint32_t pk = pack_bf16x2(a[0], a[1]);
-    *reinterpret_cast<uint32_t*>(s.y + t * s.ldy + c) = pk;
-    v0 = bf16_lo(pk);
-    v1 = bf16_hi(pk);
-  }
-  vals[2 * lane] = v0;  // columns past d_local hold 0, which adds nothing
-  vals[2 * lane + 1] = v1;
-  __syncthreads();
-  const float* h = vals + (lane & 1) * 64;
-  float acc_s = 0.0f;
+// Split-k reduction, one workgroup per token, one wavefront per 128-column
+// chunk (wavefront w takes chunks w, w + waves, ...): each lane adds two
+// columns' k-slice sums in ascending slice order and rounds them once to bf16
+// (y); the chunk's statistic follows the tile epilogue's tree (two ascending
+// FMA chains over the chunk's halves, first + second); after a barrier the
+// chunk statistics of each segment are added in ascending chunk order.
+constexpr int kMaxSplitChunks = 2048;  // 128-column chunks of both segments
+constexpr int kMaxSplits = 16;         // slices: (row tiles) x (slices) <= 16
+constexpr int kReduceWaves = 16;
+template <int SPLITS>
+__global__ __launch_bounds__(64 * kReduceWaves) void qkn_proj_reduce(const ProjParams p) {
+  __shared__ float vals[kReduceWaves][kChunkN];
+  __shared__ float chunk_sum[kMaxSplitChunks];
+  const int64_t t = blockIdx.x;
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int waves = static_cast<int>(blockDim.x) >> 6;
+  const int total = p.seg[0].nchunks + (p.nseg == 2 ? p.seg[1].nchunks : 0);
+  const int64_t slice = p.T * p.ncols;
+  float* v = vals[wave];
+  for (int g = wave; g < total; g += waves) {
+    const int si = (g >= p.seg[0].nchunks) ? 1 : 0;
+    const ProjSegDev& s = p.seg[si];
+    const int q = g - (si ? p.seg[0].nchunks : 0);
+    const int c = q * kChunkN + 2 * lane;  // d_local is a multiple of 8: c < d means c + 1 < d
+    float v0 = 0.0f, v1 = 0.0f;
+    if (c < s.d) {
+      const float* src = p.part + t * p.ncols + s.col0 + c;
+      f32x2 b[SPLITS];  // every slice's load in flight before the first add
 #pragma unroll
-  for (int i = 0; i < 64; ++i) acc_s = __builtin_fmaf(h[i], h[i], acc_s);
-  const float other = __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc_s), 0xB1, 0xF, 0xF, false));
-  if (lane == 0) s.tile_partials[static_cast<int64_t>(q) * p.T + t] = acc_s + other;
+      for (int k = 0; k < SPLITS; ++k) b[k] = *reinterpret_cast<const f32x2*>(src + k * slice);
+      f32x2 a = b[0];
+#pragma unroll
+      for (int k = 1; k < SPLITS; ++k) {
+        a[0] = a[0] + b[k][0];
+        a[1] = a[1] + b[k][1];
+      }
+      const uint32_t pk = pack_bf16x2(a[0], a[1]);
+      *reinterpret_cast<uint32_t*>(s.y + t * s.ldy + c) = pk;
+      v0 = bf16_lo(pk);
+      v1 = bf16_hi(pk);
+    }
+    v[2 * lane] = v0;  // columns past d_local hold 0, which adds nothing
+    v[2 * lane + 1] = v1;
+    // the wavefront's own LDS row: a wavefront-scope fence orders the writes
+    // before the other lanes' reads (no workgroup barrier in a loop whose
+    // trip count differs between wavefronts)
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    const float* h = v + (lane & 1) * 64;
+    float acc_s = 0.0f;
+#pragma unroll 16
+    for (int i = 0; i < 64; ++i) acc_s = __builtin_fmaf(h[i], h[i], acc_s);
+    const float other = __builtin_bit_cast(
+        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc_s), 0xB1, 0xF, 0xF, false));
+    if (lane == 0) chunk_sum[g] = acc_s + other;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();  // the row is read before the next chunk overwrites it
+  }
+  __syncthreads();
+  if (tid < p.nseg) {
+    const ProjSegDev& s = p.seg[tid];
+    const float* cs = chunk_sum + (tid ? p.seg[0].nchunks : 0);
+    float S = cs[0];
+    for (int n = 1; n < s.nchunks; ++n) S = S + cs[n];
+    s.partials[t] = S;
+  }
 }
 
 // partials[t] = chunk statistics of token t added in ascending chunk order.
@@ -621,7 +649,7 @@ const TileShape& choose_tile() {
 // columns or the segments -- so Q and K launched together or apart, and any
 // device, give the same bits.
 constexpr int64_t kSplitMaxRowTiles = 8;
-constexpr int64_t kSplitRowSlices = 16;
+constexpr int64_t kSplitRowSlices = kMaxSplits;
 constexpr int kSplitBk = 64;
 constexpr int kSplitStages = 4;  // a 256-deep slice has all its loads in flight at once
 
@@ -641,18 +669,20 @@ Plan plan_of(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg) {
   }
   pl.splits = 1;
   pl.kslice = static_cast<int>(hidden);
-  if (g_tile_choice == 0 && pl.m_tiles <= kSplitMaxRowTiles) {
+  if (g_tile_choice == 0 && pl.m_tiles <= kSplitMaxRowTiles && pl.chunks <= kMaxSplitChunks) {
     int splits = 1;
     while (pl.m_tiles * splits * 2 <= kSplitRowSlices && hidden >= int64_t{128} * splits * 2)
       splits *= 2;
     if (splits > 1) {
+      // slices of ceil(hidden / splits) rounded up to a multiple of 8: all
+      // `splits` of them non-empty, since hidden / splits >= 128 > 7 (splits - 1)
       const int64_t per = (hidden + splits - 1) / splits;
-      pl.kslice = static_cast<int>((per + kSplitBk - 1) / kSplitBk * kSplitBk);
-      pl.splits = static_cast<int>((hidden + pl.kslice - 1) / pl.kslice);
+      pl.kslice = static_cast<int>((per + 7) / 8 * 8);
+      pl.splits = splits;
     }
   }
-  pl.ws_bytes = 4 * T * pl.chunks;  // chunk statistics
-  if (pl.splits > 1) pl.ws_bytes += 4 * int64_t{pl.splits} * T * pl.ncols;  // slice products
+  pl.ws_bytes = pl.splits > 1 ? 4 * int64_t{pl.splits} * T * pl.ncols  // slice sums
+                              : 4 * T * pl.chunks;                    // chunk statistics
 
   return pl;
 }
@@ -740,7 +770,6 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   p.ncols = static_cast<int32_t>(pl.ncols);
   float* ws = static_cast<float*>(workspace);
   p.part = split ? ws : nullptr;
-  if (split) ws += int64_t{pl.splits} * T * pl.ncols;
   int32_t tile0 = 0, col0 = 0;
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
@@ -754,8 +783,8 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     d.tile0 = tile0;
     d.col0 = col0;
     d.nchunks = static_cast<int32_t>(chunks_of(s.d_local));
-    d.tile_partials = ws;
-    ws += static_cast<int64_t>(d.nchunks) * T;
+    d.tile_partials = split ? nullptr : ws;
+    if (!split) ws += static_cast<int64_t>(d.nchunks) * T;
     tile0 += static_cast<int32_t>((s.d_local + ts.bn - 1) / ts.bn);
     col0 += static_cast<int32_t>(s.d_local);
   }
@@ -777,14 +806,21 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   if (hipLaunchKernel(gemm, dim3(static_cast<unsigned>(grid)), dim3(kThreads), args, 0, st) !=
       hipSuccess)
     return QKN_EHIP;
-  if (split && hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_reduce),
-                               dim3(static_cast<unsigned>(pl.chunks), static_cast<unsigned>(T)),
-                               dim3(64), args, 0, st) != hipSuccess)
-    return QKN_EHIP;
-  const dim3 fgrid(static_cast<unsigned>((T + 255) / 256), static_cast<unsigned>(nseg));
-  if (hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_finish), fgrid, dim3(256), args, 0,
-                      st) != hipSuccess)
-    return QKN_EHIP;
+  if (split) {
+    const int waves = pl.chunks < kReduceWaves ? static_cast<int>(pl.chunks) : kReduceWaves;
+    const void* reduce = pl.splits == 2   ? reinterpret_cast<const void*>(qkn_proj_reduce<2>)
+                         : pl.splits == 4 ? reinterpret_cast<const void*>(qkn_proj_reduce<4>)
+                         : pl.splits == 8 ? reinterpret_cast<const void*>(qkn_proj_reduce<8>)
+                                          : reinterpret_cast<const void*>(qkn_proj_reduce<16>);
+    if (hipLaunchKernel(reduce,
+                        dim3(static_cast<unsigned>(T)), dim3(64 * waves), args, 0, st) != hipSuccess)
+      return QKN_EHIP;
+  } else {
+    const dim3 fgrid(static_cast<unsigned>((T + 255) / 256), static_cast<unsigned>(nseg));
+    if (hipLaunchKernel(reinterpret_cast<const void*>(qkn_proj_finish), fgrid, dim3(256), args,
+                        0, st) != hipSuccess)
+      return QKN_EHIP;
+  }
   qkn_host::record_launch(info);
   return QKN_OK;
 }

@@ -496,9 +496,9 @@ def test_proj_workspace_size(lib):
     assert lib.qkn_proj_workspace_bytes(8192, 4096, segs, 2) == 4 * 8192 * (16 + 5)
     assert lib.qkn_proj_workspace_bytes(8192, 4096, segs, 1) == 4 * 8192 * 16
     # decode: one row tile -> 16 slices of 256 (row tiles x slices <= 16, slices >= 128
-    # deep): the slices' fp32 products, then the chunk statistics
+    # deep): the slices' fp32 sums
     def split_ws(T, splits, ncols, chunks):
-        return 4 * splits * T * ncols + 4 * T * chunks
+        return 4 * splits * T * ncols
     assert lib.qkn_proj_workspace_bytes(64, 4096, segs, 2) == split_ws(64, 16, 2048 + 520, 21)
     assert lib.qkn_proj_workspace_bytes(64, 4096, segs, 1) == split_ws(64, 16, 2048, 16)
     # the slice count depends on T and hidden only
