@@ -270,13 +270,19 @@ int qkn_last_launch(qkn_launch_info* info);
  * Process-wide tuning knobs (for benchmarks and tests; not thread-safe with
  * concurrent launches). Keys:
  *   "waves_per_cu"   wavefronts per CU used to size the grid (0 = the
- *                    default: enough to keep ~24 KB (bf16) or ~32 KB (fp8)
+ *                    default: enough to keep ~24 KB (bf16) or ~28 KB (fp8)
  *                    of rows requested per CU, at least 6, at most the
  *                    occupancy limit; larger values oversubscribe, which is
  *                    correct but not persistent);
  *   "prefetch"       1 = pipelined kernels that request the next token
- *                    before writing the current one (bf16 register path),
- *                    0 = not (default);
+ *                    before writing the current one (bf16 register path,
+ *                    modes without a wait), 0 = not (default);
+ *   "wait_schedule"  the waiting kernels' order of work per wavefront:
+ *                    0 = token by token (publish, x * gamma, wait, store),
+ *                    1 = the same with the next token's rows and first poll
+ *                    requested early, 2 = publish ahead (default): a token's
+ *                    statistics are published one token before it waits for
+ *                    the other ranks'; same results;
  *   "balance"        1 = shrink the grid so every wavefront takes the same
  *                    number of tokens, 0 = use the full grid (default);
  *   "token_blocks"   1 = each wavefront takes a contiguous range of tokens,

@@ -395,24 +395,38 @@ __device__ __forceinline__ void store_scaled(const DevSeg& s, int64_t col, int64
 // round's epoch in the high half, written by a single aligned 64-bit store, so
 // a reader that sees the epoch also sees the value (no separate flag or fence).
 
-__device__ __forceinline__ void publish_slot(uint64_t* slot, float v, uint32_t epoch) {
+// The slots are written and read through buffer instructions with the sc1
+// policy, the form the memory model gives agent-scope relaxed atomic loads and
+// stores. (Not flat instructions: a flat access in flight makes the compiler
+// wait for every outstanding load before the next use of any of them, which
+// would undo the schedules that keep rows requested across a wait.)
+constexpr int kCoherentCpol = 16;  // sc1: bypass the CU-local cache
+
+typedef unsigned int B64 __attribute__((ext_vector_type(2)));  // the 64-bit buffer operand
+
+// Lane 0 publishes `v` with `epoch` at byte address `at` (one aligned 64-bit store).
+__device__ __forceinline__ void publish_slot_at(uintptr_t at, float v, uint32_t epoch, int lane) {
   const uint64_t word = (static_cast<uint64_t>(epoch) << 32) | __builtin_bit_cast(uint32_t, v);
-  __hip_atomic_store(slot, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(B64, word),
+                                        make_rsrc(reinterpret_cast<const void*>(at), 8),
+                                        lane == 0 ? 0 : 8, 0, kCoherentCpol);
 }
 
-// Lanes 0..tp-1 other than `rank` poll rank k's slot of token t until it
-// carries `epoch`, at most `limit` times (with a short sleep between polls).
-// A lane that gives up, or any lane once `given_up` is set, returns NaN.
-// `first` is the slot's word as read when the token's rows were requested (see
-// poll_slots); only a lane whose slot was not ready yet polls again.
-__device__ __forceinline__ float wait_slot(const uint64_t* slots, int64_t T, int64_t t, int lane,
+// Lanes 0..tp-1 other than `rank` poll rank k's slot of the token (byte
+// address `at` + 8 k T, `nrec` bytes behind `at`) until it carries `epoch`, at
+// most `limit` times (with a short sleep between polls). A lane that gives up,
+// or any lane once `given_up` is set, returns NaN. `first` is the slot's word
+// as read by the token's first poll; only a lane whose slot was not ready yet
+// polls again.
+__device__ __forceinline__ float wait_slot(uintptr_t at, uint32_t nrec, int64_t T, int lane,
                                            int tp, int rank, uint32_t epoch, int64_t limit,
                                            bool given_up, uint64_t first, bool& gave_up_now) {
   float v = 0.0f;
   if (lane < tp && lane != rank) {
     v = __builtin_nanf("");
     if (!given_up) {
-      const uint64_t* slot = slots + static_cast<int64_t>(lane) * T + t;
+      const Rsrc r = make_rsrc(reinterpret_cast<const void*>(at), nrec);
+      const int off = static_cast<int>(lane * T * 8);
       uint64_t word = first;
       for (int64_t n = 1;;) {
         if (static_cast<uint32_t>(word >> 32) == epoch) {
@@ -424,14 +438,19 @@ __device__ __forceinline__ float wait_slot(const uint64_t* slots, int64_t T, int
           break;
         }
         __builtin_amdgcn_s_sleep(1);
-        word = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        word = __builtin_bit_cast(uint64_t,
+                                  __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherentCpol));
       }
     }
   }
   return v;
 }
 
-constexpr int kCoherentCpol = 16;  // sc1: bypass the CU-local cache
+// Lane 0 sets the launch's status word (agent-coherent 32-bit store).
+__device__ __forceinline__ void set_status(int* status, int value, int lane) {
+  __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(value), make_rsrc(status, 4),
+                                        lane == 0 ? 0 : 4, 0, kCoherentCpol);
+}
 
 // The rank a wavefront computes and where that rank's slice sits: the launch's
 // rank with no offsets, or, when one launch runs every rank of a group, rank
@@ -536,7 +555,10 @@ __device__ __forceinline__ void store_scaled_at(uintptr_t row, uint32_t bytes, i
 }
 
 // `live` false (a pipelined request past the last token): nothing is fetched.
-template <class F, int N0, int N1, int MODE>
+// POLL false (wait mode, publish-ahead schedule): the rows only; the first poll
+// of the token's slots is issued later, once the other ranks have had time to
+// publish.
+template <class F, int N0, int N1, int MODE, bool POLL = true>
 __device__ __forceinline__ void fetch_token(const KParams& p, const Cursor& c,
                                             const CursorBytes& nb, int lane, int own_rank,
                                             TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
@@ -550,11 +572,65 @@ __device__ __forceinline__ void fetch_token(const KParams& p, const Cursor& c,
     r.slots0 = load_slots_at(c.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, live);
     if constexpr (N1 > 0) r.slots1 = load_slots_at(c.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, live);
   }
-  if constexpr (MODE == kFusedWait) {
+  r.word0 = 0;
+  r.word1 = 0;
+  if constexpr (MODE == kFusedWait && POLL) {
     r.word0 = poll_slots_at(c.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, live);
-    r.word1 = 0;
     if constexpr (N1 > 0) r.word1 = poll_slots_at(c.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, live);
   }
+}
+
+// Wait mode, Phase A of the token in `r`: the wavefront's statistics, which
+// lane 0 publishes to this rank's flagged slots.
+template <class F, int N0, int N1>
+__device__ __forceinline__ void publish_token(const KParams& p, const Cursor& c, int lane,
+                                              const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r,
+                                              float& own0, float& own1) {
+  own0 = wave_sum(row_lane_sumsq<F, N0>(r.x0));
+  own1 = 0.0f;
+  if constexpr (N1 > 0) own1 = wave_sum(row_lane_sumsq<F, N1>(r.x1));
+  publish_slot_at(c.own[0], own0, p.epoch, lane);
+  if constexpr (N1 > 0) publish_slot_at(c.own[1], own1, p.epoch, lane);
+}
+
+// Wait mode, Phases B and C of the token in `r` whose own statistics are
+// published: x * gamma, then the other ranks' statistics (`word0/1`: the first
+// poll of their slots; lanes whose slot was not ready poll again, bounded),
+// the combination, the factor and the stores.
+template <class F, int N0, int N1>
+__device__ __forceinline__ void finish_waiting_token(
+    const KParams& p, const Cursor& c, const CursorBytes& nb, int lane, int own_rank,
+    const f32x4 (&g0)[N0][kGammaVecs<F>], const f32x4 (&g1)[(N1 > 0 ? N1 : 1)][kGammaVecs<F>],
+    const TokenRegs<N0, (N1 > 0 ? N1 : 1)>& r, float own0, float own1, uint64_t word0,
+    uint64_t word1, bool& given_up) {
+  constexpr int M1 = N1 > 0 ? N1 : 1;
+  // Phase B, compute path: independent of the statistics.
+  float z0[N0][F::kPer];
+  float z1[M1][F::kPer];
+  times_gamma<F, N0>(r.x0, g0, z0);
+  if constexpr (N1 > 0) times_gamma<F, N1>(r.x1, g1, z1);
+  // Phase B, reduction path.
+  bool gave_up = false;
+  const float slots0 = wait_slot(c.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, p.epoch,
+                                 p.spin_limit, given_up, word0, gave_up);
+  float slots1 = 0.0f;
+  if constexpr (N1 > 0)
+    slots1 = wait_slot(c.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, p.epoch, p.spin_limit,
+                       given_up || gave_up, word1, gave_up);
+  if (__ballot(gave_up) != 0) {
+    if (!given_up) set_status(p.status, 1, lane);
+    given_up = true;  // later tokens of this wavefront do not wait again
+  }
+  const float inv0 = rms_inverse(combine_slots(slots0, own0, p.tp, own_rank), p.seg[0].rcp_d_full,
+                                 p.eps);
+  float inv1 = 0.0f;
+  if constexpr (N1 > 0)
+    inv1 = rms_inverse(combine_slots(slots1, own1, p.tp, own_rank), p.seg[1].rcp_d_full, p.eps);
+  // Phase C.
+  store_scaled_at<F, N0>(c.y[0], nb.row[0], lane, z0, inv0);
+  if constexpr (N1 > 0) store_scaled_at<F, N1>(c.y[1], nb.row[1], lane, z1, inv1);
+  st4f_lane0(inv0, rsrc_of(c.inv[0], nb.inv[0]), lane);
+  if constexpr (N1 > 0) st4f_lane0(inv1, rsrc_of(c.inv[1], nb.inv[1]), lane);
 }
 
 // Phases A, B and C of the token at cursor `c`, whose rows and slots are in `r`.
@@ -568,6 +644,14 @@ __device__ __forceinline__ void process_token(const KParams& p, const Cursor& c,
   constexpr int M1 = N1 > 0 ? N1 : 1;
   const DevSeg& s0 = p.seg[0];
   const DevSeg& s1 = p.seg[1];
+  if constexpr (MODE == kFusedWait) {
+    // publish this rank's statistics before waiting for the others'
+    float own0, own1;
+    publish_token<F, N0, N1>(p, c, lane, r, own0, own1);
+    finish_waiting_token<F, N0, N1>(p, c, nb, lane, own_rank, g0, g1, r, own0, own1, r.word0,
+                                    r.word1, given_up);
+    return;
+  }
 
   // Phase A: per-lane partial sums (not needed when every slot is given).
   float a0 = 0.0f, a1 = 0.0f;
@@ -581,19 +665,12 @@ __device__ __forceinline__ void process_token(const KParams& p, const Cursor& c,
     st4f_lane0(own0, rsrc_of(c.own[0], nb.own[0]), lane);
   } else if constexpr (MODE == kPublish) {
     const float own0 = wave_sum(a0);
-    if (lane == 0) publish_slot(reinterpret_cast<uint64_t*>(c.own[0]), own0, p.epoch);
+    publish_slot_at(c.own[0], own0, p.epoch, lane);
   } else {
     float own0 = 0.0f, own1 = 0.0f;
-    if constexpr (MODE == kFused || MODE == kFusedWait) {
+    if constexpr (MODE == kFused) {
       own0 = wave_sum(a0);
       if constexpr (N1 > 0) own1 = wave_sum(a1);
-    }
-    if constexpr (MODE == kFusedWait) {
-      // publish this rank's statistics before waiting for the others'
-      if (lane == 0) {
-        publish_slot(reinterpret_cast<uint64_t*>(c.own[0]), own0, p.epoch);
-        if constexpr (N1 > 0) publish_slot(reinterpret_cast<uint64_t*>(c.own[1]), own1, p.epoch);
-      }
     }
 
     // Phase B, compute path: independent of the statistic.
@@ -603,20 +680,7 @@ __device__ __forceinline__ void process_token(const KParams& p, const Cursor& c,
     if constexpr (N1 > 0) times_gamma<F, N1>(r.x1, g1, z1);
 
     // Phase B, reduction path.
-    float slots0 = r.slots0, slots1 = r.slots1;
-    if constexpr (MODE == kFusedWait) {
-      bool gave_up = false;
-      slots0 = wait_slot(reinterpret_cast<const uint64_t*>(c.sl[0]), p.T, 0, lane, p.tp, own_rank,
-                         p.epoch, p.spin_limit, given_up, r.word0, gave_up);
-      if constexpr (N1 > 0)
-        slots1 = wait_slot(reinterpret_cast<const uint64_t*>(c.sl[1]), p.T, 0, lane, p.tp, own_rank,
-                           p.epoch, p.spin_limit, given_up || gave_up, r.word1, gave_up);
-      if (__ballot(gave_up) != 0) {
-        if (!given_up && lane == 0)
-          __hip_atomic_store(p.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        given_up = true;  // later tokens of this wavefront do not wait again
-      }
-    }
+    const float slots0 = r.slots0, slots1 = r.slots1;
     const float S0 = combine_slots(slots0, own0, p.tp, own_rank);
     const float inv0 = rms_inverse(S0, s0.rcp_d_full, p.eps);
     float inv1 = 0.0f;
@@ -729,7 +793,53 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
   CursorBytes nb;
   make_cursors<F, MODE>(p, ws, t, step, c, dc, nb);
   TokenRegs<N0, M1> ra;
-  fetch_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, ra);
+  if constexpr (SCHED == 2) {
+    static_assert(MODE == kFusedWait, "the publish-ahead schedule is a wait-mode schedule");
+    // Publish ahead: a token's statistics are published one token before it
+    // waits for the other ranks' (its rows requested two tokens before), so
+    // that by the time a wavefront polls, its peers -- which run the same
+    // schedule -- have usually published long since. Step with token X
+    // current, Y next and Z the one after: issue X's first poll, request Z's
+    // rows (after the poll, so that waiting for the poll, which the in-order
+    // memory counter measures, does not wait for Z), publish Y, then wait for
+    // X's peers and finish X. Three register
+    // sets take the three roles in turn (the loop is unrolled by three, so no
+    // copy waits on requests in flight). Waits still move only to tokens
+    // whose peers published before waiting themselves, so with every
+    // wavefront resident no chain of waits can close.
+    TokenRegs<N0, M1> rb, rcc;
+    const int64_t last = end - 1;
+    fetch_token<F, N0, N1, MODE, false>(p, c, nb, lane, own_rank, ra);
+    Cursor cb = c, cc = c;
+    advance(cb, dc);
+    fetch_token<F, N0, N1, MODE, false>(p, cb, nb, lane, own_rank, rb, t + step <= last);
+    float oa0 = 0.0f, oa1 = 0.0f, ob0 = 0.0f, ob1 = 0.0f, oc0 = 0.0f, oc1 = 0.0f;
+    publish_token<F, N0, N1>(p, c, lane, ra, oa0, oa1);
+#define QKN_PA_STEP(cx, rx, ox0, ox1, cy, ry, oy0, oy1, cz, rz)                                 \
+  {                                                                                             \
+    const bool live_y = t + step <= last;                                                       \
+    const uint64_t w0_ = poll_slots_at(cx.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, true);    \
+    uint64_t w1_ = 0;                                                                           \
+    if constexpr (N1 > 0) w1_ = poll_slots_at(cx.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, true); \
+    cz = cy;                                                                                    \
+    advance(cz, dc);                                                                            \
+    fetch_token<F, N0, N1, MODE, false>(p, cz, nb, lane, own_rank, rz, t + 2 * step <= last);   \
+    if (live_y) publish_token<F, N0, N1>(p, cy, lane, ry, oy0, oy1);                            \
+    finish_waiting_token<F, N0, N1>(p, cx, nb, lane, own_rank, g0, g1, rx, ox0, ox1, w0_, w1_,  \
+                                    given_up);                                                  \
+    if (!live_y) break;                                                                         \
+    t += step;                                                                                  \
+  }
+    while (true) {
+      QKN_PA_STEP(c, ra, oa0, oa1, cb, rb, ob0, ob1, cc, rcc)
+      QKN_PA_STEP(cb, rb, ob0, ob1, cc, rcc, oc0, oc1, c, ra)
+      QKN_PA_STEP(cc, rcc, oc0, oc1, c, ra, oa0, oa1, cb, rb)
+    }
+#undef QKN_PA_STEP
+    return;
+  } else {
+    fetch_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, ra);
+  }
   if constexpr (PF) {
     TokenRegs<N0, M1> rb;
     const int64_t last = end - 1;
@@ -974,7 +1084,9 @@ enum Format { kBf16 = 0, kFp8 = 1 };
 // Register-path grid (measured on MI355X, prefill shards of 8192 and 32768
 // tokens): bf16 peaks with about 24 KB of rows requested per CU in one-wave
 // workgroups; fp8 rows are half as long and need more of them in flight,
-// about 32 KB per CU, best spread in four-wave workgroups.
+// about 28 KB per CU (12 wavefronts for both shards' row lengths; 16, which
+// 32 KB gave the 32768-token shard, ran 5 % slower), best spread in four-wave
+// workgroups.
 struct FormatInfo {
   int esz;                 // bytes per element
   int per;                 // elements per 16-byte chunk
@@ -985,7 +1097,7 @@ struct FormatInfo {
   int waves_per_block;     // register path: default workgroup size in wavefronts
 };
 constexpr FormatInfo kFormat[2] = {{2, 8, 8, {16, 32}, "", 24 * 1024, 1},
-                                   {1, 16, 4, {8, 16}, "_fp8", 32 * 1024, 4}};
+                                   {1, 16, 4, {8, 16}, "_fp8", 28 * 1024, 4}};
 
 // Chunks per lane are rounded up to 1, 2, 4 or 8; unused chunks are masked.
 constexpr int kNIdx[9] = {-1, 0, 1, 2, 2, 3, 3, 3, 3};  // chunks/lane -> table index
@@ -1014,8 +1126,10 @@ const RowsFn kFusedTable[2][4][5] = {QKN_FULL_SET(FmtBf16, kFused, 0),
 const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(FmtBf16, kApply, 0), QKN_ONE_SET(FmtBf16, kApply, 1)};
 const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(FmtBf16, kPartial, 0),
                                     QKN_ONE_SET(FmtBf16, kPartial, 1)};
-const RowsFn kFusedWaitTable[2][4][5] = {QKN_FULL_SET(FmtBf16, kFusedWait, 0),
-                                         QKN_FULL_SET(FmtBf16, kFusedWait, 1)};
+// wait mode: 0 and 1 as above, 2 publish-ahead
+const RowsFn kFusedWaitTable[3][4][5] = {QKN_FULL_SET(FmtBf16, kFusedWait, 0),
+                                         QKN_FULL_SET(FmtBf16, kFusedWait, 1),
+                                         QKN_FULL_SET(FmtBf16, kFusedWait, 2)};
 const RowsFn kPublishTable[4] = QKN_ONE_SET(FmtBf16, kPublish, 0);
 // fp8: [N0 index][N1 index]
 const RowsFn kFusedTable8[4][5] = QKN_FULL_SET8(kFused);
@@ -1044,13 +1158,14 @@ const char* const kModeName[5] = {"fused", "apply", "partial", "fused_wait", "pu
 
 // Static names "rows<N0,N1>/mode" ("rows_pf<...>" when pipelined, "rows_fp8<...>" for fp8).
 const char* rows_name(int fmt, int mode, int sched, int i0, int i1) {
-  static char names[2][5][2][4][5][40];
+  static char names[2][5][3][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
-    const char* const prefix[2][2] = {{"rows", "rows_pf"}, {"rows_fp8", "rows_pf_fp8"}};
+    const char* const prefix[2][3] = {{"rows", "rows_pf", "rows_pa"},
+                                      {"rows_fp8", "rows_pf_fp8", "rows_pa_fp8"}};
     for (int fm = 0; fm < 2; ++fm)
       for (int m = 0; m < 5; ++m)
-        for (int f = 0; f < 2; ++f)
+        for (int f = 0; f < 3; ++f)
           for (int a = 0; a < 4; ++a)
             for (int b = 0; b < 5; ++b)
               snprintf(names[fm][m][f][a][b], sizeof(names[fm][m][f][a][b]), "%s<%d,%d>/%s",
@@ -1080,6 +1195,7 @@ const char* wide_name(int fmt, int mode, int i0, int i1) {
 
 // Options.
 int64_t g_opt_waves_per_cu = 0;
+int64_t g_opt_wait_schedule = 2;  // publish ahead
 int64_t g_opt_waves_per_block = 0;
 int64_t g_opt_force_generic = 0;
 int64_t g_opt_validate_only = 0;
@@ -1329,7 +1445,7 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
     name = wide_name(fmt, mode, wide_i0, wide_i1);
     lds = (mode == kPartial) ? 0 : static_cast<int>(gamma_floats * 4);
   } else if (waits) {
-    const int sched = (mode == kFusedWait && g_opt_prefetch) ? 1 : 0;
+    const int sched = (mode == kFusedWait) ? static_cast<int>(g_opt_wait_schedule) : 0;
     if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[sched][idx[0]][i1]);
     else fn = reinterpret_cast<const void*>(kPublishTable[idx[0]]);
     name = rows_name(fmt, mode, sched, idx[0], i1);
@@ -1700,6 +1816,9 @@ int qkn_set_option(const char* key, int64_t value) {
   } else if (strcmp(key, "prefetch") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_prefetch = value;
+  } else if (strcmp(key, "wait_schedule") == 0) {
+    if (value < 0 || value > 2) return QKN_EINVAL;
+    g_opt_wait_schedule = value;
   } else if (strcmp(key, "balance") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_balance = value;

@@ -89,7 +89,27 @@ GROUPS = [workloads.DECODE_TP4, workloads.DECODE_TP8, workloads.PREFILL_TP2.with
 @pytest.mark.parametrize("wl", GROUPS, ids=lambda w: w.name)
 def test_whole_group_in_one_launch(wl):
     """Every rank of the group in one launch: each wavefront publishes its rank's
-    statistic and waits for the others'; all of them are resident at once."""
+    statistic and waits for the others'; all of them are resident at once.
+    Default schedule: each token's statistics published one token ahead."""
+    info = _run_group_and_check(wl)
+    assert info["kernel"].startswith("rows_pa<"), info
+
+
+@pytest.mark.parametrize("sched", [0, 1])
+@pytest.mark.parametrize("wl", [workloads.DECODE_TP4, workloads.PREFILL_TP2.with_tokens(2048)],
+                         ids=lambda w: w.name)
+def test_whole_group_token_by_token_schedules(wl, sched):
+    """The same with the token-by-token schedules (publish, then wait, per
+    token; 1 also requests the next token early): identical results."""
+    L.qkn_set_option("wait_schedule", sched)
+    try:
+        info = _run_group_and_check(wl)
+        assert info["kernel"].startswith("rows_pf<" if sched else "rows<"), info
+    finally:
+        L.qkn_set_option("wait_schedule", 2)
+
+
+def _run_group_and_check(wl):
     data = inputs(wl)
     slots = _slot_arrays(wl)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
@@ -112,6 +132,7 @@ def test_whole_group_in_one_launch(wl):
             cols = workloads.shard_cols(d_full, wl.tp, r)
             assert np.array_equal(bits_of(s.y[:, cols]), ref[t]["y"]), (r, t)
             assert np.array_equal(s.inv_rms[r].cpu().numpy(), ref[t]["inv"]), (r, t)
+    return info
 
 
 def test_timeout_when_nobody_publishes():
