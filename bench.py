@@ -211,6 +211,27 @@ def time_launches(torch, fn, steps, warmup):
     return start.elapsed_time(end), [a.elapsed_time(b) for a, b in ev]
 
 
+def stream_copy_ms(torch, L, nbytes: int, min_footprint: int, steps: int, warmup: int,
+                   grids=(2048, 4096, 8192, 16384)):
+    """Best time (ms) per launch of the streaming copy (qkn_calib_copy) of
+    `nbytes` bytes in total (half read, half written) over rotating buffer sets
+    of at least `min_footprint` bytes, and its grid: the practical ceiling of a
+    read-once/write-once kernel moving the same bytes."""
+    half = nbytes // 2 // 16 * 16
+    nbuf = max(2, -(-min_footprint // (2 * half)))
+    bufs = [(torch.empty(half, dtype=torch.uint8, device="cuda:0"),
+             torch.empty(half, dtype=torch.uint8, device="cuda:0")) for _ in range(nbuf)]
+    best = None
+    for blocks in grids:
+        r = time_region(torch, lambda i, b=blocks: L.qkn_calib_copy(*bufs[i % nbuf], blocks=b),
+                        steps, warmup) / steps
+        if best is None or r < best[0]:
+            best = (r, blocks)
+    del bufs
+    torch.cuda.synchronize()
+    return best
+
+
 def time_graph(torch, fn, per_graph, replays):
     """Mean time (ms) per call when `per_graph` calls are replayed from one HIP graph."""
     fn(0)
@@ -505,7 +526,19 @@ def main():
         extras["calibration_copy"] = {"read_bytes": xq.numel() * 2, "write_bytes": yq.numel() * 2,
                                       "launches": 5}
     if not args.no_extras:
-        # plain copy of the same bytes (x -> y of both tensors), torch's copy kernel
+        # the practical ceiling: a streaming copy of the same bytes in one launch
+        # (qkn_calib_copy, best of four grid sizes), over rotating buffer sets as
+        # large as the kernel's, so that it too reads from HBM
+        copy_bytes = sum(2 * s.x.numel() * 2 for s in case.sets[0])  # read + written
+        cms, cblocks = stream_copy_ms(torch, L, copy_bytes, min_fp, args.steps, args.warmup)
+        extras["stream_copy_same_bytes"] = {
+            "bytes": copy_bytes, "us_per_step": round(cms * 1e3, 3), "blocks": cblocks,
+            "gbs": round(copy_bytes / (cms * 1e-3) / 1e9, 1),
+            "fused_kernel_frac_of_copy": round(cms / ms_per_step, 4)}
+        # the launch floor: an empty kernel replayed from a HIP graph
+        us = time_graph(torch, lambda i: L.qkn_calib_empty(), 200, 10) * 1e3
+        extras["empty_kernel_graph"] = {"us_per_launch_graph": round(us, 3)}
+        # torch's copy of the same tensors (two launches), for context
         csets = [([s.x for s in segs], [s.y for s in segs]) for segs in case.sets]
 
         def copy(i):
@@ -513,9 +546,9 @@ def main():
             for a, b in zip(xs, ys):
                 b.copy_(a)
         r = time_region(torch, copy, args.steps, args.warmup)
-        copy_bytes = sum(2 * s.x.numel() * 2 for s in case.sets[0])
-        extras["copy_same_bytes"] = {"bytes": copy_bytes, "us_per_step": round(r / args.steps * 1e3, 3),
-                                     "gbs": round(copy_bytes / (r / args.steps * 1e-3) / 1e9, 1)}
+        extras["torch_copy_same_bytes"] = {"bytes": copy_bytes,
+                                           "us_per_step": round(r / args.steps * 1e3, 3),
+                                           "gbs": round(copy_bytes / (r / args.steps * 1e-3) / 1e9, 1)}
         # two launches per tensor: Phase A, then Phases B+C (x read twice)
         r = time_region(torch, case.launch_two_step, args.steps, args.warmup)
         two_bytes = case.bytes + sum(2 * s.x.numel() for s in case.sets[0])
@@ -528,6 +561,9 @@ def main():
         extras["full_vector_tp1"] = {"kernel": L.qkn_last_launch()["kernel"], "bytes": fcase.bytes,
                                      "kernel_us": round(fk * 1e3, 3),
                                      "gbs": round(fcase.bytes / (fk * 1e-3) / 1e9, 1)}
+        cms, _ = stream_copy_ms(torch, L, fcase.bytes, min_fp, args.steps, args.warmup)
+        extras["full_vector_tp1"]["copy_us"] = round(cms * 1e3, 3)
+        extras["full_vector_tp1"]["frac_of_copy"] = round(cms / fk, 4)
         del fcase
         # the Phase B wait: every rank of the tp group in one launch, each wavefront
         # publishing its statistic and waiting for the others' (same data as tp = 1)
@@ -558,6 +594,9 @@ def main():
         extras["long_prefill_tp4"] = {"kernel": L.qkn_last_launch()["kernel"], "bytes": lcase.bytes,
                                       "kernel_us": round(lk * 1e3, 3),
                                       "gbs": round(lcase.bytes / (lk * 1e-3) / 1e9, 1)}
+        cms, _ = stream_copy_ms(torch, L, lcase.bytes, min_fp, nl, 5)
+        extras["long_prefill_tp4"]["copy_us"] = round(cms * 1e3, 3)
+        extras["long_prefill_tp4"]["frac_of_copy"] = round(cms / lk, 4)
         del lcase
         # FP8-E4M3 activations (Sec. IV-C's second format): the same prefill
         # shard, and the decode shape replayed from a graph
@@ -568,6 +607,9 @@ def main():
                                        "kernel_us": round(pk * 1e3, 3),
                                        "gbs": round(p8.bytes / (pk * 1e-3) / 1e9, 1),
                                        "frac_of_peak": round(p8.bytes / (pk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        cms, _ = stream_copy_ms(torch, L, p8.bytes, min_fp, args.steps, args.warmup)
+        extras["fp8_prefill_shard"]["copy_us"] = round(cms * 1e3, 3)
+        extras["fp8_prefill_shard"]["frac_of_copy"] = round(cms / pk, 4)
         del p8
         d8 = Case(workloads.DECODE_TP4.with_dtype("fp8"), 0, 0, torch, L, workloads)
         us = time_graph(torch, lambda i, c=d8: c.launch(0), 200, 10) * 1e3

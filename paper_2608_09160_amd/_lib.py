@@ -88,6 +88,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qkn_proj_workspace_bytes.restype = _c_i64
     lib.qkn_proj_partial.argtypes = [_vp, _c_i64, _c_i64, _c_i64, ctypes.POINTER(QknProjSeg),
                                      ctypes.c_int, _vp, _c_i64, _vp]
+    lib.qkn_calib_copy.argtypes = [_vp, _vp, _c_i64, _c_i64, _vp]
+    lib.qkn_calib_empty.argtypes = [_vp]
     lib.qkn_strerror.argtypes = [ctypes.c_int]
     lib.qkn_strerror.restype = ctypes.c_char_p
     lib.qkn_last_launch.argtypes = [ctypes.POINTER(QknLaunchInfo)]
@@ -95,7 +97,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("qkn_partial_sumsq", "qkn_apply", "qkn_fused_shard", "qkn_full",
                  "qkn_last_launch", "qkn_set_option", "qkn_publish_partials",
                  "qkn_fused_shard_wait", "qkn_fused_group_wait", "qkn_partial_sumsq_fp8",
-                 "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8", "qkn_proj_partial"):
+                 "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8", "qkn_proj_partial",
+                 "qkn_calib_copy", "qkn_calib_empty"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -439,6 +442,23 @@ class PreparedProj:
                                           len(self.segs), self.workspace.data_ptr(),
                                           self.workspace.numel(), _stream(stream)),
                "qkn_proj_partial")
+
+
+def qkn_calib_copy(x: torch.Tensor, y: torch.Tensor, blocks: int = 2048, stream=None) -> None:
+    """Streaming copy of x's bytes into y (both contiguous, same byte size):
+    the measurement reference of a read-once/write-once kernel."""
+    if not (x.is_contiguous() and y.is_contiguous()):
+        raise ValueError("qkn_calib_copy: contiguous tensors only")
+    nbytes = x.numel() * x.element_size()
+    if y.numel() * y.element_size() != nbytes:
+        raise ValueError("qkn_calib_copy: x and y differ in size")
+    _check(load().qkn_calib_copy(x.data_ptr(), y.data_ptr(), nbytes, blocks, _stream(stream)),
+           "qkn_calib_copy")
+
+
+def qkn_calib_empty(stream=None) -> None:
+    """An empty kernel: the launch floor."""
+    _check(load().qkn_calib_empty(_stream(stream)), "qkn_calib_empty")
 
 
 def qkn_last_launch() -> dict:

@@ -15,7 +15,7 @@ import sys
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG_DIR)
-SOURCES = [os.path.join(PKG_DIR, "csrc", name) for name in ("qkn.hip", "qkn_proj.hip")]
+SOURCES = [os.path.join(PKG_DIR, "csrc", name) for name in ("qkn.hip", "qkn_proj.hip", "qkn_calib.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG_DIR, "libqkn.so")
 ARCH = "gfx950"

@@ -578,3 +578,19 @@ def test_proj_tile_option(lib):
     assert lib.qkn_set_option(b"proj_tile", 3) == L.QKN_EINVAL
     assert lib.qkn_set_option(b"proj_tile", -1) == L.QKN_EINVAL
     assert lib.qkn_set_option(b"proj_tile", 0) == 0
+
+
+def test_calib_validation(dry):
+    X, Y = BASE, BASE + 64 * MB
+    assert dry.qkn_calib_copy(X, Y, 1 << 20, 2048, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "calib_copy"
+    assert dry.qkn_calib_copy(X, Y, 0, 2048, None) == 0                  # nothing to copy
+    assert dry.qkn_calib_copy(X, Y, 24, 2048, None) == L.QKN_EINVAL      # not whole 16-byte vectors
+    assert dry.qkn_calib_copy(X, Y, -16, 2048, None) == L.QKN_EINVAL
+    assert dry.qkn_calib_copy(X, Y, 1 << 20, 0, None) == L.QKN_EINVAL
+    assert dry.qkn_calib_copy(X, Y, 1 << 20, 65537, None) == L.QKN_EINVAL
+    assert dry.qkn_calib_copy(X + 8, Y, 1 << 20, 2048, None) == L.QKN_EINVAL
+    assert dry.qkn_calib_copy(None, Y, 1 << 20, 2048, None) == L.QKN_EINVAL
+    assert dry.qkn_calib_copy(X, X + (1 << 19), 1 << 20, 2048, None) == L.QKN_EOVERLAP
+    assert dry.qkn_calib_empty(None) == 0
+    assert L.qkn_last_launch()["kernel"] == "calib_empty"
