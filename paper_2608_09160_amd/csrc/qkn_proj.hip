@@ -85,7 +85,7 @@ struct ProjParams {
   int64_t ldx;
   int64_t T;
   int32_t hidden;
-  int32_t m_tiles;
+  int32_t m_tiles;       // row tiles (of the launch's tile height)
   int32_t n_tiles;       // column tiles of all segments
   int32_t nseg;
   ProjSegDev seg[2];
@@ -124,12 +124,13 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) {
 
 // Tile in the grouped order -> (row tile, column tile): groups of kGroupM row
 // tiles, each sweeping all column tiles.
-__device__ __forceinline__ bool tile_from(int logical, const ProjParams& p, int& mt, int& nt) {
-  if (logical >= p.m_tiles * p.n_tiles) return false;
+__device__ __forceinline__ bool tile_from(int logical, int m_tiles, const ProjParams& p, int& mt,
+                                          int& nt) {
+  if (logical >= m_tiles * p.n_tiles) return false;
   const int group_size = kGroupM * p.n_tiles;
   const int group = logical / group_size;
   const int first_m = group * kGroupM;
-  const int gm = (p.m_tiles - first_m < kGroupM) ? p.m_tiles - first_m : kGroupM;
+  const int gm = (m_tiles - first_m < kGroupM) ? m_tiles - first_m : kGroupM;
   const int in_group = logical - group * group_size;
   mt = first_m + in_group % gm;
   nt = in_group / gm;
@@ -138,10 +139,11 @@ __device__ __forceinline__ bool tile_from(int logical, const ProjParams& p, int&
 
 // Tile number -> (row tile, column tile): XCD-contiguous runs, then groups of
 // kGroupM row tiles sweeping all column tiles.
-__device__ __forceinline__ bool tile_of(int bid, int grid, const ProjParams& p, int& mt, int& nt) {
+__device__ __forceinline__ bool tile_of(int bid, int grid, int m_tiles, const ProjParams& p, int& mt,
+                                        int& nt) {
   const int per_xcd = grid / kXcds;  // the grid is a multiple of kXcds
   const int logical = (bid % kXcds) * per_xcd + bid / kXcds;
-  return tile_from(logical, p, mt, nt);
+  return tile_from(logical, m_tiles, p, mt, nt);
 }
 
 // Epilogue of a (64 WMB) x (64 WNB) tile: round the fp32 accumulators once to
@@ -188,21 +190,25 @@ __device__ __forceinline__ void epilogue(const ProjParams& p, const ProjSegDev& 
   // Phase A per 128-column chunk: thread pair (2u, 2u+1) takes one row of one
   // chunk, columns [0, 64) and [64, 128) of it in ascending order; the pair adds.
   constexpr int kUnits = BM * (BN / kChunkN) * 2;
+  static_assert(kUnits % 64 == 0, "whole wavefronts of units");
 #pragma unroll
-  for (int it = 0; it < kUnits / kThreads; ++it) {
+  for (int it = 0; it < (kUnits + kThreads - 1) / kThreads; ++it) {
     const int u = tid + kThreads * it;
+    const bool live = u < kUnits;  // a 64-row tile has units for half the threads
     const int half = u & 1, rc = u >> 1;
     const int row = rc % BM, chunk = rc / BM;
     const uint16_t* src = out + row * OUT_ROW + chunk * kChunkN + half * 64;
     float acc_s = 0.0f;
+    if (live) {
 #pragma unroll
-    for (int c = 0; c < 64; c += 8) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(src + c);
+      for (int c = 0; c < 64; c += 8) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(src + c);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float lo = bf16_lo(v[e]), hi = bf16_hi(v[e]);
-        acc_s = __builtin_fmaf(lo, lo, acc_s);
-        acc_s = __builtin_fmaf(hi, hi, acc_s);
+        for (int e = 0; e < 4; ++e) {
+          const float lo = bf16_lo(v[e]), hi = bf16_hi(v[e]);
+          acc_s = __builtin_fmaf(lo, lo, acc_s);
+          acc_s = __builtin_fmaf(hi, hi, acc_s);
+        }
       }
     }
     // the partner lane's sum (quad_perm [1,0,3,2]: lanes 2u and 2u+1 swap)
@@ -212,7 +218,7 @@ __device__ __forceinline__ void epilogue(const ProjParams& p, const ProjSegDev& 
     const float second = half ? acc_s : other;
     const float chunk_sum = first + second;
     const int gchunk = n0 / kChunkN + chunk;  // chunk index within the segment
-    if (half == 0 && row < rows_a && gchunk < s.nchunks)
+    if (live && half == 0 && row < rows_a && gchunk < s.nchunks)
       s.tile_partials[static_cast<int64_t>(gchunk) * p.T + m0 + row] = chunk_sum;
   }
 }
@@ -245,7 +251,8 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
   using C = TileCfg<WMB, WNB, BK>;
   __shared__ __align__(16) uint16_t lds[C::kLds];
   int mt, nt;
-  if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p, mt, nt)) return;
+  if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p.m_tiles, p, mt, nt))
+    return;
   const int si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
   const ProjSegDev& s = p.seg[si];
   const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
@@ -356,21 +363,23 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
 // per row, which puts the 16 rows read by a 16-lane group at 16 distinct
 // 16-byte bank groups. Lane l of a load instruction therefore fetches the
 // global k-vector that belongs at its fixed LDS slot.
-template <int BK, int S>
+template <int WMB, int BK, int S>
 struct DlCfg {
-  static constexpr int BM = 128, BN = 128;
+  static constexpr int BM = 64 * WMB, BN = 128;        // tile rows (tokens), columns
   static constexpr int P = BK / 8;                     // 16-byte slots per row
   static constexpr int kRowsPerGroup = 16 / P;         // rows sharing a swizzle value
   static constexpr int kRowBytes = BK * 2;
-  static constexpr int kTileBytes = BM * kRowBytes;    // one operand tile (BM == BN)
-  static constexpr int kStageBytes = 2 * kTileBytes;   // A then B
+  static constexpr int kTileBytesA = BM * kRowBytes;
+  static constexpr int kTileBytesB = BN * kRowBytes;
+  static constexpr int kStageBytes = kTileBytesA + kTileBytesB;  // A then B
   static constexpr int kOutRow = BN + 8;
   static constexpr int kLdsBytes =
       (S * kStageBytes > BM * kOutRow * 2) ? S * kStageBytes : BM * kOutRow * 2;
-  static constexpr int kLoadsPerTile = kTileBytes / 1024;      // 1 KB per wave instruction
-  static constexpr int kLoadsPerWave = kLoadsPerTile / 4;      // per operand tile
+  static constexpr int kLoadsA = kTileBytesA / 1024 / 4;  // 1 KB wave instructions per wave
+  static constexpr int kLoadsB = kTileBytesB / 1024 / 4;
   static constexpr int kRowsPerLoad = 1024 / kRowBytes;
-  static_assert(kLoadsPerTile % 4 == 0, "whole load instructions per wavefront");
+  static_assert(kTileBytesA % 4096 == 0 && kTileBytesB % 4096 == 0,
+                "whole load instructions per wavefront");
   static_assert(kLdsBytes <= 160 * 1024, "LDS");
 };
 
@@ -398,29 +407,18 @@ __device__ __forceinline__ void vm_wait(int n) {
   }
 }
 
-// SPLIT: workgroup b takes k-slice b mod splits of tile b / splits and adds
-// its fp32 products into the partial sums instead of running the epilogue.
-template <int BK, int S, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p) {
-  using C = DlCfg<BK, S>;
-  __shared__ __align__(1024) unsigned char lds[C::kLdsBytes];
-  int mt, nt;
-  int k_lo = 0, k_hi = p.hidden;
-  if constexpr (SPLIT) {
-    const int b = static_cast<int>(blockIdx.x);
-    if (!tile_from(b / p.splits, p, mt, nt)) return;
-    k_lo = (b % p.splits) * p.kslice;
-    k_hi = (k_lo + p.kslice < p.hidden) ? k_lo + p.kslice : p.hidden;
-  } else {
-    if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p, mt, nt)) return;
-  }
-  const int si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
-  const ProjSegDev& s = p.seg[si];
-  const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
-  const int n0 = (nt - s.tile0) * C::BN;
-  const int rows_a = static_cast<int>((p.T - m0 < C::BM) ? p.T - m0 : C::BM);
-  const int rows_b = (s.d - n0 < C::BN) ? s.d - n0 : C::BN;
-
+// Main loop of one direct-to-LDS tile: BM = 64 WMB rows from m0 (rows_a of
+// them valid) by 128 columns from n0 of segment s (rows_b valid), k in
+// [k_lo, k_hi). Four wavefronts in a 2 x 2 grid, each (32 WMB) x 64, i.e.
+// WMB x 2 MFMA blocks of 32 x 32; every accumulator takes its k-blocks of 16
+// in ascending order whatever the tile's height, so all tile shapes give the
+// same bits.
+template <int WMB, int BK, int S>
+__device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDev& s,
+                                            unsigned char* lds, int64_t m0, int n0, int rows_a,
+                                            int rows_b, int k_lo, int k_hi,
+                                            f32x16 (&acc)[WMB][2]) {
+  using C = DlCfg<WMB, BK, S>;
   const int tid = static_cast<int>(threadIdx.x);
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -432,33 +430,40 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
   const Rsrc rb = make_rsrc(s.w + static_cast<int64_t>(n0) * s.ldw, b_bytes);
 
   // this lane's global row offset and k-vector for each of the wave's loads
-  uint32_t a_row[C::kLoadsPerWave], b_row[C::kLoadsPerWave];
-  int kvec[C::kLoadsPerWave];
+  uint32_t a_row[C::kLoadsA], b_row[C::kLoadsB];
+  int kva[C::kLoadsA], kvb[C::kLoadsB];
 #pragma unroll
-  for (int i = 0; i < C::kLoadsPerWave; ++i) {
-    const int row = (wave * C::kLoadsPerWave + i) * C::kRowsPerLoad + lane / C::P;
-    const int slot = lane % C::P;
-    kvec[i] = (slot ^ ((row / C::kRowsPerGroup) % C::P)) * 8;
+  for (int i = 0; i < C::kLoadsA; ++i) {
+    const int row = (wave * C::kLoadsA + i) * C::kRowsPerLoad + lane / C::P;
+    kva[i] = ((lane % C::P) ^ ((row / C::kRowsPerGroup) % C::P)) * 8;
     a_row[i] = static_cast<uint32_t>(row * p.ldx * 2);
+  }
+#pragma unroll
+  for (int i = 0; i < C::kLoadsB; ++i) {
+    const int row = (wave * C::kLoadsB + i) * C::kRowsPerLoad + lane / C::P;
+    kvb[i] = ((lane % C::P) ^ ((row / C::kRowsPerGroup) % C::P)) * 8;
     b_row[i] = static_cast<uint32_t>(row * s.ldw * 2);
   }
-  // Stage `stage` (k from k0) into its ring slot.
+  // Stage `stage` (k from k0) into its ring slot; a k-vector past k_hi is
+  // moved past the descriptor and reads zeros.
 #define QKN_ISSUE_STAGE(stage, k0)                                                          \
   do {                                                                                      \
     const int base_ = ((stage) % S) * C::kStageBytes;                                       \
-    _Pragma("unroll") for (int i_ = 0; i_ < C::kLoadsPerWave; ++i_) {                       \
-      const int k_ = (k0) + kvec[i_];                                                       \
-      const int slice_ = base_ + (wave * C::kLoadsPerWave + i_) * 1024;                     \
-      load16_to_lds(ra, (LdsByte*)(lds + slice_),                                           \
+    _Pragma("unroll") for (int i_ = 0; i_ < C::kLoadsA; ++i_) {                             \
+      const int k_ = (k0) + kva[i_];                                                        \
+      load16_to_lds(ra, (LdsByte*)(lds + base_ + (wave * C::kLoadsA + i_) * 1024),          \
                     k_ < k_hi ? a_row[i_] + static_cast<uint32_t>(k_ * 2) : a_bytes);        \
-      load16_to_lds(rb, (LdsByte*)(lds + C::kTileBytes + slice_),                           \
+    }                                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < C::kLoadsB; ++i_) {                             \
+      const int k_ = (k0) + kvb[i_];                                                        \
+      load16_to_lds(rb,                                                                     \
+                    (LdsByte*)(lds + base_ + C::kTileBytesA + (wave * C::kLoadsB + i_) * 1024), \
                     k_ < k_hi ? b_row[i_] + static_cast<uint32_t>(k_ * 2) : b_bytes);        \
     }                                                                                       \
   } while (0)
 
-  f32x16 acc[2][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < WMB; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -471,7 +476,7 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
 
   const int frag_row = lane & 31;
   const int frag_kv = lane >> 5;
-  constexpr int kPerStage = 2 * C::kLoadsPerWave;  // load instructions per wave per stage
+  constexpr int kPerStage = C::kLoadsA + C::kLoadsB;  // load instructions per wave per stage
   for (int kt = 0; kt < nk; ++kt) {
     // stages kt + 1 .. kt + S - 2 may stay in flight
     const int later = (nk - 1 - kt < S - 2) ? nk - 1 - kt : S - 2;
@@ -483,47 +488,109 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
     __builtin_amdgcn_s_barrier();
     if (kt + S - 1 < nk) QKN_ISSUE_STAGE(kt + S - 1, k_lo + (kt + S - 1) * BK);
     const unsigned char* a = lds + (kt % S) * C::kStageBytes;
-    const unsigned char* b = a + C::kTileBytes;
+    const unsigned char* b = a + C::kTileBytesA;
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       const int kv = kk / 8 + frag_kv;
-      bf16x8 af[2], bfr[2];
+      bf16x8 af[WMB], bfr[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int ra_row = wm * 64 + i * 32 + frag_row;
-        const int rb_row = wn * 64 + i * 32 + frag_row;
+      for (int i = 0; i < WMB; ++i) {
+        const int ra_row = wm * 32 * WMB + i * 32 + frag_row;
         af[i] = *reinterpret_cast<const bf16x8*>(
             a + ra_row * C::kRowBytes + ((kv ^ ((ra_row / C::kRowsPerGroup) % C::P)) * 16));
-        bfr[i] = *reinterpret_cast<const bf16x8*>(
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int rb_row = wn * 64 + j * 32 + frag_row;
+        bfr[j] = *reinterpret_cast<const bf16x8*>(
             b + rb_row * C::kRowBytes + ((kv ^ ((rb_row / C::kRowsPerGroup) % C::P)) * 16));
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < WMB; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
   }
-  if constexpr (SPLIT) {
-    // fp32 products of this k-slice: lanes 0..31 of a row are 32 adjacent columns
-    float* part = p.part + static_cast<int64_t>(static_cast<int>(blockIdx.x) % p.splits) * p.T * p.ncols;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int col = wn * 64 + j * 32 + (lane & 31);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (row < rows_a && col < rows_b)
-            part[(m0 + row) * p.ncols + s.col0 + n0 + col] = acc[i][j][r];
-        }
-      }
-  } else {
-    __syncthreads();
-    epilogue<2, 2, C::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds), m0, n0, rows_a, rows_b);
-  }
 #undef QKN_ISSUE_STAGE
+}
+
+// The segment, origin and valid extent of output tile (row tile mt of height
+// 64 WMB from row `row0`, column tile nt over both segments).
+struct TileAt {
+  int si;
+  int64_t m0;
+  int n0, rows_a, rows_b;
+};
+template <int WMB>
+__device__ __forceinline__ TileAt tile_at(const ProjParams& p, int64_t row0, int mt, int nt) {
+  TileAt t;
+  t.si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
+  const ProjSegDev& s = p.seg[t.si];
+  t.m0 = row0 + static_cast<int64_t>(mt) * (64 * WMB);
+  t.n0 = (nt - s.tile0) * 128;
+  t.rows_a = static_cast<int>((p.T - t.m0 < 64 * WMB) ? p.T - t.m0 : 64 * WMB);
+  t.rows_b = (s.d - t.n0 < 128) ? s.d - t.n0 : 128;
+  return t;
+}
+
+// One whole tile with its epilogue.
+template <int WMB, int BK, int S>
+__device__ __forceinline__ void dl_tile(const ProjParams& p, unsigned char* lds, int64_t row0,
+                                        int mt, int nt) {
+  const TileAt t = tile_at<WMB>(p, row0, mt, nt);
+  const ProjSegDev& s = p.seg[t.si];
+  f32x16 acc[WMB][2];
+  dl_mainloop<WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, 0, p.hidden, acc);
+  __syncthreads();
+  epilogue<WMB, 2, DlCfg<WMB, BK, S>::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds), t.m0,
+                                               t.n0, t.rows_a, t.rows_b);
+}
+
+// Whole 128 x 128 tiles, XCD-aware order.
+template <int BK, int S>
+__global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p) {
+  __shared__ __align__(1024) unsigned char lds[DlCfg<2, BK, S>::kLdsBytes];
+  int mt, nt;
+  if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p.m_tiles, p, mt, nt))
+    return;
+  dl_tile<2, BK, S>(p, lds, 0, mt, nt);
+}
+
+// Split k: workgroup b takes k-slice b mod splits of tile b / splits (tiles
+// of 64 WMB rows) and stores its fp32 sums into the slice array instead of
+// running the epilogue.
+template <int WMB, int BK, int S>
+__global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams p) {
+  using C = DlCfg<WMB, BK, S>;
+  __shared__ __align__(1024) unsigned char lds[C::kLdsBytes];
+  const int b = static_cast<int>(blockIdx.x);
+  int mt, nt;
+  if (!tile_from(b / p.splits, p.m_tiles, p, mt, nt)) return;
+  const int ks = b % p.splits;
+  const int k_lo = ks * p.kslice;
+  const int k_hi = (k_lo + p.kslice < p.hidden) ? k_lo + p.kslice : p.hidden;
+  const TileAt t = tile_at<WMB>(p, 0, mt, nt);
+  const ProjSegDev& s = p.seg[t.si];
+  f32x16 acc[WMB][2];
+  dl_mainloop<WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, k_lo, k_hi, acc);
+  // fp32 sums of this k-slice: lanes 0..31 of a row are 32 adjacent columns
+  const int lane = static_cast<int>(threadIdx.x) & 63;
+  const int wave = static_cast<int>(threadIdx.x) >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  float* part = p.part + static_cast<int64_t>(ks) * p.T * p.ncols;
+#pragma unroll
+  for (int i = 0; i < WMB; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 32 * WMB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row < t.rows_a && col < t.rows_b)
+          part[(t.m0 + row) * p.ncols + s.col0 + t.n0 + col] = acc[i][j][r];
+      }
+    }
 }
 
 // Split-k reduction, one workgroup per token, one wavefront per 128-column
@@ -625,7 +692,7 @@ struct TileShape {
         static_cast<int>(TileCfg<WM, WN, BK>::kLds * sizeof(uint16_t)), NAME              \
   }
 #define QKN_DL(BK, S, NAME) \
-  TileShape { qkn_proj_gemm_dl<BK, S, false>, 128, 128, BK, DlCfg<BK, S>::kLdsBytes, NAME }
+  TileShape { qkn_proj_gemm_dl<BK, S>, 128, 128, BK, DlCfg<2, BK, S>::kLdsBytes, NAME }
 // [0] is the default (measured fastest on MI355X: 128 x 128 tiles, k 64 per
 // stage, two LDS stages filled directly from global memory, two workgroups
 // per CU); [1] is the register-staged kernel.
@@ -785,15 +852,37 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     d.nchunks = static_cast<int32_t>(chunks_of(s.d_local));
     d.tile_partials = split ? nullptr : ws;
     if (!split) ws += static_cast<int64_t>(d.nchunks) * T;
-    tile0 += static_cast<int32_t>((s.d_local + ts.bn - 1) / ts.bn);
+    tile0 += static_cast<int32_t>((s.d_local + 127) / 128);  // every kernel's tiles are 128 wide
     col0 += static_cast<int32_t>(s.d_local);
   }
   p.n_tiles = tile0;
-  const int64_t tiles = static_cast<int64_t>(p.m_tiles) * p.n_tiles;
-  if (tiles * pl.splits > 0x7fffffff - kXcds) return QKN_ENOTSUP;
-  const int64_t grid = split ? tiles * pl.splits : (tiles + kXcds - 1) / kXcds * kXcds;
-  const char* name = split ? "proj<128x128,64,dl4,splitk>" : ts.name;
-  const int lds = split ? DlCfg<kSplitBk, kSplitStages>::kLdsBytes : ts.lds_bytes;
+  const auto round8 = [](int64_t v) { return (v + kXcds - 1) / kXcds * kXcds; };
+  const int64_t max_wgs = 0x7fffffff - 2 * kXcds;
+  int64_t grid = 0;
+  const char* name = ts.name;
+  int lds = ts.lds_bytes;
+  const void* gemm = reinterpret_cast<const void*>(ts.fn);
+  if (split) {
+    // 64-row tiles when every token fits in one: half the A loads and MFMAs
+    const bool half = T <= 64;
+    p.m_tiles = static_cast<int32_t>(half ? 1 : (T + 127) / 128);
+    const int64_t tiles = static_cast<int64_t>(p.m_tiles) * p.n_tiles;
+    if (tiles * pl.splits > max_wgs) return QKN_ENOTSUP;
+    grid = tiles * pl.splits;
+    if (half) {
+      gemm = reinterpret_cast<const void*>(qkn_proj_gemm_split<1, kSplitBk, kSplitStages>);
+      name = "proj<64x128,64,dl4,splitk>";
+      lds = DlCfg<1, kSplitBk, kSplitStages>::kLdsBytes;
+    } else {
+      gemm = reinterpret_cast<const void*>(qkn_proj_gemm_split<2, kSplitBk, kSplitStages>);
+      name = "proj<128x128,64,dl4,splitk>";
+      lds = DlCfg<2, kSplitBk, kSplitStages>::kLdsBytes;
+    }
+  } else {
+    const int64_t tiles = static_cast<int64_t>(p.m_tiles) * p.n_tiles;
+    if (tiles > max_wgs) return QKN_ENOTSUP;
+    grid = round8(tiles);
+  }
   const qkn_launch_info info{name, grid, kThreads, grid * (kThreads / 64), lds};
   if (qkn_host::validate_only()) {
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, info.lds_bytes});
@@ -801,8 +890,6 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* args[] = {&p};
-  const void* gemm = split ? reinterpret_cast<const void*>(qkn_proj_gemm_dl<kSplitBk, kSplitStages, true>)
-                           : reinterpret_cast<const void*>(ts.fn);
   if (hipLaunchKernel(gemm, dim3(static_cast<unsigned>(grid)), dim3(kThreads), args, 0, st) !=
       hipSuccess)
     return QKN_EHIP;

@@ -572,6 +572,34 @@ def dry_proj_ok(lib, *args):
         assert lib.qkn_set_option(b"validate_only", 0) == 0
 
 
+def _proj_plan(lib, T, hidden, dims):
+    """The kernel qkn_proj_partial chooses for these shapes (validate-only: planned for 256 CUs)."""
+    X, W, Y, P, WS = BASE, BASE + 64 * MB, BASE + 1024 * MB, BASE + 2048 * MB, BASE + 3072 * MB
+    segs = [_pseg(W + i * 256 * MB, hidden, Y + i * 256 * MB, d, P + i * MB, d)
+            for i, d in enumerate(dims)]
+    need = lib.qkn_proj_workspace_bytes(T, hidden, (L.QknProjSeg * len(segs))(*segs), len(segs))
+    assert dry_proj_ok(lib, X, hidden, T, hidden, segs, WS, need)
+    return L.qkn_last_launch()["kernel"]
+
+
+def test_proj_plan(lib):
+    # whole 128 x 128 tiles at prefill sizes
+    assert _proj_plan(lib, 8192, 4096, (2048, 512)) == "proj<128x128,64,dl2>"
+    assert _proj_plan(lib, 1025, 4096, (1024,)) == "proj<128x128,64,dl2>"
+    # decode sizes split k, with 64-row tiles up to 64 tokens
+    assert _proj_plan(lib, 64, 4096, (1024, 256)) == "proj<64x128,64,dl4,splitk>"
+    assert _proj_plan(lib, 1, 4096, (1024,)) == "proj<64x128,64,dl4,splitk>"
+    assert _proj_plan(lib, 65, 4096, (1024, 256)) == "proj<128x128,64,dl4,splitk>"
+    assert _proj_plan(lib, 1024, 4096, (1024, 256)) == "proj<128x128,64,dl4,splitk>"
+    # a forced kernel never splits
+    assert lib.qkn_set_option(b"proj_tile", 2) == 0
+    try:
+        assert _proj_plan(lib, 8192, 4096, (2048, 512)) == "proj<128x128,64,reg>"
+        assert _proj_plan(lib, 64, 4096, (1024, 256)) == "proj<128x128,64,reg>"
+    finally:
+        assert lib.qkn_set_option(b"proj_tile", 0) == 0
+
+
 def test_proj_tile_option(lib):
     for v in (0, 1, 2):
         assert lib.qkn_set_option(b"proj_tile", v) == 0

@@ -224,3 +224,4 @@ def test_split_k_against_one_slice(T, hidden):
     again, _ = _run(x, ws)
     for a, b in zip(again, split):
         assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
