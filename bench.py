@@ -192,6 +192,22 @@ def time_each(torch, fn, steps, warmup):
     return [a.elapsed_time(b) for a, b in ev]
 
 
+def time_cold(torch, fn, steps, flush):
+    """Per-call durations (ms) from events right around each call, every call
+    preceded (outside the events) by `flush()`, which evicts the caches."""
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        flush()
+        ev[i][0].record(stream)
+        fn(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
 def time_launches(torch, fn, steps, warmup):
     """(region ms, per-call ms list) -- per-call events inside one timed region."""
     stream = torch.cuda.current_stream()
@@ -587,6 +603,29 @@ def main():
                          "grid": L.qkn_last_launch()["grid"], "bytes": dcase.bytes}
             del dcase
         extras["decode_latency_warm"] = lat
+        # cold: every launch after a streaming copy of 2 x 384 MB, which evicts
+        # L2 and the 256 MB Infinity Cache; events right around each launch,
+        # next to the same measurement of an empty kernel (the events' own cost)
+        big = 384 << 20
+        fa = torch.empty(big, dtype=torch.uint8, device="cuda:0")
+        fb = torch.empty(big, dtype=torch.uint8, device="cuda:0")
+
+        def flush():
+            L.qkn_calib_copy(fa, fb, blocks=8192)
+        nc = 100
+        empty = np.array(time_cold(torch, lambda i: L.qkn_calib_empty(), nc, flush)) * 1e3
+        cold = {"empty_kernel_event_us_median": round(float(np.median(empty)), 3)}
+        for name in ("decode_T64_q4096_k1024_tp4", "decode_T256_q5120_k1024_tp8"):
+            dwl = workloads.WORKLOADS[name]
+            dcase = Case(dwl, 0, 0, torch, L, workloads, partials=dwl.tp > 1)
+            t = np.array(time_cold(torch, lambda i, c=dcase: c.launch(0), nc, flush)) * 1e3
+            cold[name] = {"event_us_median": round(float(np.median(t)), 3),
+                          "event_us_p10": round(float(np.percentile(t, 10)), 3),
+                          "event_us_p90": round(float(np.percentile(t, 90)), 3),
+                          "over_empty_kernel_us": round(float(np.median(t) - np.median(empty)), 3)}
+            del dcase
+        del fa, fb
+        extras["decode_latency_cold"] = cold
         # long prefill shard
         lcase = Case(workloads.LONG_PREFILL_TP4, 0, min_fp, torch, L, workloads)
         nl = max(20, args.steps // 4)
