@@ -34,6 +34,12 @@
 //     tile's 128 columns is summed from the staged bf16 values (two ascending
 //     FMA chains of 64 columns, added). A second launch adds the per-tile
 //     statistics of each token in ascending tile order.
+//   * Decode-sized launches (at most 8 row tiles, which alone would leave most
+//     CUs idle) split k: separate workgroups take contiguous k-slices of each
+//     tile (64-row tiles up to 64 tokens; four LDS stages, so a slice's loads
+//     are all in flight at once) and store their fp32 sums; one reduction
+//     launch, a workgroup per token, adds the slices in ascending order,
+//     rounds once, writes y and takes the statistic with the same tree.
 
 #include <hip/hip_runtime.h>
 
@@ -713,8 +719,9 @@ const TileShape& choose_tile() {
 // at most kSplitMaxRowTiles row tiles (1024 tokens). The slice count is the
 // largest power of two with (row tiles) x (slices) <= kSplitRowSlices and
 // slices at least 128 deep. It depends on T and hidden only -- not on the
-// columns or the segments -- so Q and K launched together or apart, and any
-// device, give the same bits.
+// columns or the segments (launches of more than kMaxSplitChunks 128-column
+// chunks in all, 262144 columns, are not split) -- so Q and K launched
+// together or apart, and any device, give the same bits.
 constexpr int64_t kSplitMaxRowTiles = 8;
 constexpr int64_t kSplitRowSlices = kMaxSplits;
 constexpr int kSplitBk = 64;
