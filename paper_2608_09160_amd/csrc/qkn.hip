@@ -837,6 +837,47 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
     }
 #undef QKN_PA_STEP
     return;
+  } else if constexpr (SCHED == 3) {
+    static_assert(MODE == kFusedWait, "the publish-ahead schedule is a wait-mode schedule");
+    // Publish two ahead: as above with four tokens in registers -- X waits and
+    // is finished, Y was published a step ago, Z is published now, W's rows
+    // are requested -- so a peer may lag two tokens before anyone waits.
+    TokenRegs<N0, M1> rb, rcc, rd;
+    const int64_t last = end - 1;
+    fetch_token<F, N0, N1, MODE, false>(p, c, nb, lane, own_rank, ra);
+    Cursor cb = c, cc = c, cd = c;
+    advance(cb, dc);
+    fetch_token<F, N0, N1, MODE, false>(p, cb, nb, lane, own_rank, rb, t + step <= last);
+    cc = cb;
+    advance(cc, dc);
+    fetch_token<F, N0, N1, MODE, false>(p, cc, nb, lane, own_rank, rcc, t + 2 * step <= last);
+    float oa0 = 0.0f, oa1 = 0.0f, ob0 = 0.0f, ob1 = 0.0f, oc0 = 0.0f, oc1 = 0.0f, od0 = 0.0f,
+          od1 = 0.0f;
+    publish_token<F, N0, N1>(p, c, lane, ra, oa0, oa1);
+    if (t + step <= last) publish_token<F, N0, N1>(p, cb, lane, rb, ob0, ob1);
+#define QKN_PA2_STEP(cx, rx, ox0, ox1, cy, ry, cz, rz, oz0, oz1, cw, rw)                         \
+  {                                                                                             \
+    const bool live_y = t + step <= last;                                                       \
+    const uint64_t w0_ = poll_slots_at(cx.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, true);    \
+    uint64_t w1_ = 0;                                                                           \
+    if constexpr (N1 > 0) w1_ = poll_slots_at(cx.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, true); \
+    cw = cz;                                                                                    \
+    advance(cw, dc);                                                                            \
+    fetch_token<F, N0, N1, MODE, false>(p, cw, nb, lane, own_rank, rw, t + 3 * step <= last);   \
+    if (t + 2 * step <= last) publish_token<F, N0, N1>(p, cz, lane, rz, oz0, oz1);              \
+    finish_waiting_token<F, N0, N1>(p, cx, nb, lane, own_rank, g0, g1, rx, ox0, ox1, w0_, w1_,  \
+                                    given_up);                                                  \
+    if (!live_y) break;                                                                         \
+    t += step;                                                                                  \
+  }
+    while (true) {
+      QKN_PA2_STEP(c, ra, oa0, oa1, cb, rb, cc, rcc, oc0, oc1, cd, rd)
+      QKN_PA2_STEP(cb, rb, ob0, ob1, cc, rcc, cd, rd, od0, od1, c, ra)
+      QKN_PA2_STEP(cc, rcc, oc0, oc1, cd, rd, c, ra, oa0, oa1, cb, rb)
+      QKN_PA2_STEP(cd, rd, od0, od1, c, ra, cb, rb, ob0, ob1, cc, rcc)
+    }
+#undef QKN_PA2_STEP
+    return;
   } else {
     fetch_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, ra);
   }
@@ -1126,10 +1167,10 @@ const RowsFn kFusedTable[2][4][5] = {QKN_FULL_SET(FmtBf16, kFused, 0),
 const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(FmtBf16, kApply, 0), QKN_ONE_SET(FmtBf16, kApply, 1)};
 const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(FmtBf16, kPartial, 0),
                                     QKN_ONE_SET(FmtBf16, kPartial, 1)};
-// wait mode: 0 and 1 as above, 2 publish-ahead
-const RowsFn kFusedWaitTable[3][4][5] = {QKN_FULL_SET(FmtBf16, kFusedWait, 0),
-                                         QKN_FULL_SET(FmtBf16, kFusedWait, 1),
-                                         QKN_FULL_SET(FmtBf16, kFusedWait, 2)};
+// wait mode: 0 and 1 as above, 2 publish one token ahead, 3 two tokens ahead
+const RowsFn kFusedWaitTable[4][4][5] = {
+    QKN_FULL_SET(FmtBf16, kFusedWait, 0), QKN_FULL_SET(FmtBf16, kFusedWait, 1),
+    QKN_FULL_SET(FmtBf16, kFusedWait, 2), QKN_FULL_SET(FmtBf16, kFusedWait, 3)};
 const RowsFn kPublishTable[4] = QKN_ONE_SET(FmtBf16, kPublish, 0);
 // fp8: [N0 index][N1 index]
 const RowsFn kFusedTable8[4][5] = QKN_FULL_SET8(kFused);
@@ -1158,14 +1199,14 @@ const char* const kModeName[5] = {"fused", "apply", "partial", "fused_wait", "pu
 
 // Static names "rows<N0,N1>/mode" ("rows_pf<...>" when pipelined, "rows_fp8<...>" for fp8).
 const char* rows_name(int fmt, int mode, int sched, int i0, int i1) {
-  static char names[2][5][3][4][5][40];
+  static char names[2][5][4][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
-    const char* const prefix[2][3] = {{"rows", "rows_pf", "rows_pa"},
-                                      {"rows_fp8", "rows_pf_fp8", "rows_pa_fp8"}};
+    const char* const prefix[2][4] = {{"rows", "rows_pf", "rows_pa", "rows_pa2"},
+                                      {"rows_fp8", "rows_pf_fp8", "rows_pa_fp8", "rows_pa2_fp8"}};
     for (int fm = 0; fm < 2; ++fm)
       for (int m = 0; m < 5; ++m)
-        for (int f = 0; f < 3; ++f)
+        for (int f = 0; f < 4; ++f)
           for (int a = 0; a < 4; ++a)
             for (int b = 0; b < 5; ++b)
               snprintf(names[fm][m][f][a][b], sizeof(names[fm][m][f][a][b]), "%s<%d,%d>/%s",
@@ -1195,7 +1236,7 @@ const char* wide_name(int fmt, int mode, int i0, int i1) {
 
 // Options.
 int64_t g_opt_waves_per_cu = 0;
-int64_t g_opt_wait_schedule = 2;  // publish ahead
+int64_t g_opt_wait_schedule = 3;  // publish two tokens ahead
 int64_t g_opt_waves_per_block = 0;
 int64_t g_opt_force_generic = 0;
 int64_t g_opt_validate_only = 0;
@@ -1817,7 +1858,7 @@ int qkn_set_option(const char* key, int64_t value) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_prefetch = value;
   } else if (strcmp(key, "wait_schedule") == 0) {
-    if (value < 0 || value > 2) return QKN_EINVAL;
+    if (value < 0 || value > 3) return QKN_EINVAL;
     g_opt_wait_schedule = value;
   } else if (strcmp(key, "balance") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;

@@ -350,7 +350,7 @@ def _k_nopart():
 def test_wait_entry_validation(dry):
     ok = _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block())
     assert ok == 0
-    assert L.qkn_last_launch()["kernel"] == "rows_pa<2,1>/fused_wait"  # publish ahead
+    assert L.qkn_last_launch()["kernel"] == "rows_pa2<2,1>/fused_wait"  # publish two ahead
     for kw in (dict(epoch=0), dict(spin_limit=0), dict(co_resident=0), dict(status=None),
                dict(status=BASE + 700 * MB + 2), dict(slots=(None, BASE + 600 * MB)),
                dict(slots=(BASE + 512 * MB + 4, BASE + 600 * MB))):
@@ -373,17 +373,17 @@ def test_wait_entry_validation(dry):
 
 def test_wait_schedule_option(dry):
     try:
-        for sched, prefix in ((0, "rows"), (1, "rows_pf"), (2, "rows_pa")):
+        for sched, prefix in ((0, "rows"), (1, "rows_pf"), (2, "rows_pa"), (3, "rows_pa2")):
             assert dry.qkn_set_option(b"wait_schedule", sched) == 0
             assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block()) == 0
             assert L.qkn_last_launch()["kernel"] == f"{prefix}<2,1>/fused_wait"
         # the option does not touch the kernels without a wait
         assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
         assert L.qkn_last_launch()["kernel"] == "rows<2,1>/fused"
-        assert dry.qkn_set_option(b"wait_schedule", 3) == L.QKN_EINVAL
+        assert dry.qkn_set_option(b"wait_schedule", 4) == L.QKN_EINVAL
         assert dry.qkn_set_option(b"wait_schedule", -1) == L.QKN_EINVAL
     finally:
-        assert dry.qkn_set_option(b"wait_schedule", 2) == 0
+        assert dry.qkn_set_option(b"wait_schedule", 3) == 0
 
 
 def test_publish_entry_validation(dry):
@@ -409,7 +409,7 @@ def test_group_entry_validation(dry):
         return dry.qkn_fused_group_wait(arr, len(segs), tp, T, ctypes.c_float(1e-6),
                                         ctypes.byref(wait), None)
     assert call([full(1024, 4)], 4, _wait_block()) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows_pa<2,0>/fused_wait"
+    assert L.qkn_last_launch()["kernel"] == "rows_pa2<2,0>/fused_wait"
     bad = full(1024, 4)
     bad.d_full = 4000
     assert call([bad], 4, _wait_block()) == L.QKN_EINVAL           # d_full != tp * d_local
