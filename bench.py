@@ -134,12 +134,17 @@ class GroupCase:
         self.wl, self.torch, self.L = wl, torch, L
         dev = "cuda:0"
 
+        fp8 = wl.dtype == "fp8"
+        esz = 1 if fp8 else 2
+
         def bf16(a):
+            if fp8:  # FP8 codes as uint8 device tensors (the binding takes either dtype)
+                return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).to(dev)
             a = np.ascontiguousarray(a, dtype=np.uint16)
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
         xs = [bf16(data["xq"]), bf16(data["xk"])]
         ws = [torch.from_numpy(data["gq"]).to(dev), torch.from_numpy(data["gk"]).to(dev)]
-        set_bytes = sum(2 * x.numel() * 2 for x in xs)
+        set_bytes = sum(2 * x.numel() * esz for x in xs)
         self.nsets = max(2, -(-min_footprint // set_bytes))
         self.sets = []
         for i in range(self.nsets):
@@ -151,7 +156,7 @@ class GroupCase:
         self.epoch = 0
         T, tp = wl.T, wl.tp
         # x read + y written, gamma, per rank: own slot written, tp - 1 slots read (8 B each)
-        self.bytes = sum(2 * T * d * 2 + 4 * d + 8 * T * tp * tp for d in (wl.q_full, wl.k_full))
+        self.bytes = sum(2 * T * d * esz + 4 * d + 8 * T * tp * tp for d in (wl.q_full, wl.k_full))
         torch.cuda.synchronize()
 
     def launch(self, i):
@@ -590,6 +595,14 @@ def main():
                                           "bytes": gcase.bytes, "kernel_us": round(gk * 1e3, 3),
                                           "gbs": round(gcase.bytes / (gk * 1e-3) / 1e9, 1),
                                           "status": gstatus}
+        del gcase
+        f8g = wl.with_dtype("fp8")
+        gcase = GroupCase(f8g, min_fp, torch, L, workloads.generate(f8g))
+        gk = time_region(torch, gcase.launch, args.steps, args.warmup) / args.steps
+        extras["fp8_group_wait_all_ranks"] = {"kernel": L.qkn_last_launch()["kernel"],
+                                              "bytes": gcase.bytes, "kernel_us": round(gk * 1e3, 3),
+                                              "gbs": round(gcase.bytes / (gk * 1e-3) / 1e9, 1),
+                                              "status": int(gcase.status.item())}
         del gcase
         # decode shapes: one launch replayed from a HIP graph (inputs cache-warm,
         # as right after the projection that produced them)

@@ -246,6 +246,20 @@ int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_
 int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float eps,
                          const qkn_wait* wait, void* stream);
 
+/*
+ * The three entry points above for FP8-E4M3 activations (qkn_seg8, uint8
+ * codes; conventions of the FP8 entry points): the published statistic of a
+ * slice equals qkn_partial_sumsq_fp8's, and the waiting kernels' results are
+ * bit-identical to qkn_fused_shard_fp8 given the same statistics. Register
+ * path: x 16-byte aligned, ldx and d_local multiples of 16, d_local <= 4096.
+ */
+int qkn_publish_partials_fp8(const uint8_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                             uint64_t* slots_out, uint32_t epoch, void* stream);
+int qkn_fused_shard_wait_fp8(const qkn_seg8* segs, int nseg, int tp, int rank, int64_t T,
+                             float eps, const qkn_wait* wait, void* stream);
+int qkn_fused_group_wait_fp8(const qkn_seg8* segs, int nseg, int tp, int64_t T, float eps,
+                             const qkn_wait* wait, void* stream);
+
 /* Static text for a status code (never NULL). */
 const char* qkn_strerror(int status);
 

@@ -80,6 +80,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                          ctypes.POINTER(QknWait), _vp]
     lib.qkn_fused_group_wait.argtypes = [ctypes.POINTER(QknSeg), ctypes.c_int, ctypes.c_int,
                                          _c_i64, ctypes.c_float, ctypes.POINTER(QknWait), _vp]
+    lib.qkn_publish_partials_fp8.argtypes = lib.qkn_publish_partials.argtypes
+    lib.qkn_fused_shard_wait_fp8.argtypes = lib.qkn_fused_shard_wait.argtypes
+    lib.qkn_fused_group_wait_fp8.argtypes = lib.qkn_fused_group_wait.argtypes
     lib.qkn_partial_sumsq_fp8.argtypes = lib.qkn_partial_sumsq.argtypes
     lib.qkn_apply_fp8.argtypes = lib.qkn_apply.argtypes
     lib.qkn_fused_shard_fp8.argtypes = lib.qkn_fused_shard.argtypes
@@ -98,7 +101,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                  "qkn_last_launch", "qkn_set_option", "qkn_publish_partials",
                  "qkn_fused_shard_wait", "qkn_fused_group_wait", "qkn_partial_sumsq_fp8",
                  "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8", "qkn_proj_partial",
-                 "qkn_calib_copy", "qkn_calib_empty"):
+                 "qkn_calib_copy", "qkn_calib_empty", "qkn_publish_partials_fp8",
+                 "qkn_fused_shard_wait_fp8", "qkn_fused_group_wait_fp8"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -283,10 +287,13 @@ def _slots(t: torch.Tensor, numel: int, what: str) -> int:
 
 def qkn_publish_partials(x: torch.Tensor, slots_out: torch.Tensor, epoch: int,
                          stream=None) -> None:
-    """Phase A of x [T, d_local], published as flagged slots (int64 [T], one per token)."""
-    px, ldx, T, d = _rows(x, "x")
-    _check(load().qkn_publish_partials(px, ldx, T, d, _slots(slots_out, T, "slots_out"),
-                                       epoch, _stream(stream)), "qkn_publish_partials")
+    """Phase A of x [T, d_local] (bf16, or FP8 codes), published as flagged
+    slots (int64 [T], one per token)."""
+    fmt = _fmt_of(x)
+    name = "qkn_publish_partials" + ("_fp8" if fmt == FP8 else "")
+    px, ldx, T, d = _rows(x, "x", fmt)
+    _check(getattr(load(), name)(px, ldx, T, d, _slots(slots_out, T, "slots_out"), epoch,
+                                 _stream(stream)), name)
 
 
 def make_wait(slots: Sequence[torch.Tensor], tp: int, T: int, epoch: int, spin_limit: int,
@@ -303,10 +310,12 @@ def qkn_fused_shard_wait(segs: Sequence[Seg], tp: int, rank: int, eps: float,
                          slots: Sequence[torch.Tensor], epoch: int, spin_limit: int,
                          co_resident: int, status: torch.Tensor, stream=None):
     """Fused QK-Norm that publishes its statistics and waits for the other ranks'."""
-    arr, T = _segs(segs, tp)
+    fmt = _fmt_of(segs[0].x)
+    name = "qkn_fused_shard_wait" + ("_fp8" if fmt == FP8 else "")
+    arr, T = _segs(segs, tp, fmt)
     wait = make_wait(slots, tp, T, epoch, spin_limit, co_resident, status)
-    _check(load().qkn_fused_shard_wait(arr, len(segs), tp, rank, T, eps, ctypes.byref(wait),
-                                       _stream(stream)), "qkn_fused_shard_wait")
+    _check(getattr(load(), name)(arr, len(segs), tp, rank, T, eps, ctypes.byref(wait),
+                                 _stream(stream)), name)
     return [s.y for s in segs]
 
 
@@ -315,14 +324,16 @@ def qkn_fused_group_wait(segs: Sequence[Seg], tp: int, eps: float,
                          status: torch.Tensor, stream=None):
     """Every rank of a tp group in one launch over the full tensors.
 
-    segs[i].x / .y are the full bf16 [T, d_full] tensors, .w the full gamma,
-    .d_full the full width; each rank's slice is d_full / tp columns. inv_rms,
-    if given, is fp32 [tp, T].
+    segs[i].x / .y are the full [T, d_full] tensors (bf16, or FP8 codes), .w
+    the full gamma, .d_full the full width; each rank's slice is d_full / tp
+    columns. inv_rms, if given, is fp32 [tp, T].
     """
-    arr = (QknSeg * len(segs))()
+    fmt = _fmt_of(segs[0].x)
+    name = "qkn_fused_group_wait" + ("_fp8" if fmt == FP8 else "")
+    arr = (QknSeg * len(segs))()  # qkn_seg and qkn_seg8 share this layout
     T = None
     for i, s in enumerate(segs):
-        px, ldx, Ts, d_full = _rows(s.x, f"seg{i}.x")
+        px, ldx, Ts, d_full = _rows(s.x, f"seg{i}.x", fmt)
         if d_full != s.d_full or d_full % tp:
             raise ValueError(f"seg{i}: x must hold the full width d_full, divisible by tp")
         T = Ts if T is None else T
@@ -330,14 +341,14 @@ def qkn_fused_group_wait(segs: Sequence[Seg], tp: int, eps: float,
             raise ValueError("all segments must have the same number of tokens")
         if s.y is None:
             s.y = torch.empty_like(s.x)
-        py, ldy, _, _ = _rows(s.y, f"seg{i}.y")
+        py, ldy, _, _ = _rows(s.y, f"seg{i}.y", fmt)
         if s.partials is not None:
             raise ValueError("statistics travel in the slots; partials must be None")
         arr[i] = QknSeg(px, ldx, _f32(s.w, f"seg{i}.w", d_full), None, py, ldy,
                         _f32(s.inv_rms, f"seg{i}.inv_rms", tp * Ts), d_full // tp, d_full)
     wait = make_wait(slots, tp, T, epoch, spin_limit, 1, status)
-    _check(load().qkn_fused_group_wait(arr, len(segs), tp, T, eps, ctypes.byref(wait),
-                                       _stream(stream)), "qkn_fused_group_wait")
+    _check(getattr(load(), name)(arr, len(segs), tp, T, eps, ctypes.byref(wait),
+                                 _stream(stream)), name)
     return [s.y for s in segs]
 
 

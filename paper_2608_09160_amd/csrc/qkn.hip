@@ -1152,13 +1152,14 @@ constexpr int kNVal[4] = {1, 2, 4, 8};
 #define QKN_FULL_SET(F, M, S) \
   {QKN_ROW_SET(F, M, 1, S), QKN_ROW_SET(F, M, 2, S), QKN_ROW_SET(F, M, 4, S), QKN_ROW_SET(F, M, 8, S)}
 // fp8: up to 4 chunks per lane, one token per step
-#define QKN_ROW_SET8(M, A)                                                                     \
-  {qkn_rows<FmtFp8, A, 0, M, 0>, qkn_rows<FmtFp8, A, 1, M, 0>, qkn_rows<FmtFp8, A, 2, M, 0>, \
-   qkn_rows<FmtFp8, A, 4, M, 0>, nullptr}
-#define QKN_FULL_SET8(M) \
-  {QKN_ROW_SET8(M, 1), QKN_ROW_SET8(M, 2), QKN_ROW_SET8(M, 4), {nullptr, nullptr, nullptr, nullptr, nullptr}}
-#define QKN_ONE_SET8(M) \
-  {qkn_rows<FmtFp8, 1, 0, M, 0>, qkn_rows<FmtFp8, 2, 0, M, 0>, qkn_rows<FmtFp8, 4, 0, M, 0>, nullptr}
+#define QKN_ROW_SET8(M, A, S)                                                                  \
+  {qkn_rows<FmtFp8, A, 0, M, S>, qkn_rows<FmtFp8, A, 1, M, S>, qkn_rows<FmtFp8, A, 2, M, S>, \
+   qkn_rows<FmtFp8, A, 4, M, S>, nullptr}
+#define QKN_FULL_SET8(M, S)                                                  \
+  {QKN_ROW_SET8(M, 1, S), QKN_ROW_SET8(M, 2, S), QKN_ROW_SET8(M, 4, S), \
+   {nullptr, nullptr, nullptr, nullptr, nullptr}}
+#define QKN_ONE_SET8(M, S) \
+  {qkn_rows<FmtFp8, 1, 0, M, S>, qkn_rows<FmtFp8, 2, 0, M, S>, qkn_rows<FmtFp8, 4, 0, M, S>, nullptr}
 
 // Schedules: 0 one token per step, 1 pipelined (next token requested early).
 // [schedule][N0 index][N1 index: 0 = single segment, then 1, 2, 4, 8]
@@ -1172,10 +1173,14 @@ const RowsFn kFusedWaitTable[4][4][5] = {
     QKN_FULL_SET(FmtBf16, kFusedWait, 0), QKN_FULL_SET(FmtBf16, kFusedWait, 1),
     QKN_FULL_SET(FmtBf16, kFusedWait, 2), QKN_FULL_SET(FmtBf16, kFusedWait, 3)};
 const RowsFn kPublishTable[4] = QKN_ONE_SET(FmtBf16, kPublish, 0);
-// fp8: [N0 index][N1 index]
-const RowsFn kFusedTable8[4][5] = QKN_FULL_SET8(kFused);
-const RowsFn kApplyTable8[4] = QKN_ONE_SET8(kApply);
-const RowsFn kPartialTable8[4] = QKN_ONE_SET8(kPartial);
+// fp8: [N0 index][N1 index]; the wait modes with [schedule] first, as for bf16
+const RowsFn kFusedTable8[4][5] = QKN_FULL_SET8(kFused, 0);
+const RowsFn kApplyTable8[4] = QKN_ONE_SET8(kApply, 0);
+const RowsFn kPartialTable8[4] = QKN_ONE_SET8(kPartial, 0);
+const RowsFn kFusedWaitTable8[4][4][5] = {
+    QKN_FULL_SET8(kFusedWait, 0), QKN_FULL_SET8(kFusedWait, 1), QKN_FULL_SET8(kFusedWait, 2),
+    QKN_FULL_SET8(kFusedWait, 3)};
+const RowsFn kPublishTable8[4] = QKN_ONE_SET8(kPublish, 0);
 const GenericFn kGenericTable[2][3] = {
     {qkn_generic<FmtBf16, kFused>, qkn_generic<FmtBf16, kApply>, qkn_generic<FmtBf16, kPartial>},
     {qkn_generic<FmtFp8, kFused>, qkn_generic<FmtFp8, kApply>, qkn_generic<FmtFp8, kPartial>}};
@@ -1430,7 +1435,6 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
   kp.rank = rank;
   kp.eps = eps;
   const bool waits = (mode == kFusedWait || mode == kPublish);
-  if (waits && fmt != kBf16) return QKN_ENOTSUP;
   if (waits) {
     kp.slots[0] = wa->slots[0];
     kp.slots[1] = wa->slots[1];
@@ -1487,8 +1491,12 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
     lds = (mode == kPartial) ? 0 : static_cast<int>(gamma_floats * 4);
   } else if (waits) {
     const int sched = (mode == kFusedWait) ? static_cast<int>(g_opt_wait_schedule) : 0;
-    if (mode == kFusedWait) fn = reinterpret_cast<const void*>(kFusedWaitTable[sched][idx[0]][i1]);
-    else fn = reinterpret_cast<const void*>(kPublishTable[idx[0]]);
+    if (mode == kFusedWait)
+      fn = reinterpret_cast<const void*>(fmt == kBf16 ? kFusedWaitTable[sched][idx[0]][i1]
+                                                      : kFusedWaitTable8[sched][idx[0]][i1]);
+    else
+      fn = reinterpret_cast<const void*>(fmt == kBf16 ? kPublishTable[idx[0]]
+                                                      : kPublishTable8[idx[0]]);
     name = rows_name(fmt, mode, sched, idx[0], i1);
   } else if (fast) {
     const int sched = (fmt == kBf16 && g_opt_prefetch) ? 1 : 0;  // pipelining: bf16 kernels only
@@ -1667,6 +1675,116 @@ int full_entry(const S* segs, int nseg, int64_t T, float eps, int fmt, void* str
   return fused_entry(segs, nseg, 1, 0, T, eps, fmt, stream);
 }
 
+int publish_impl(const void* x, int64_t ldx, int64_t T, int64_t d_local, uint64_t* slots_out,
+                 uint32_t epoch, int fmt, void* stream) {
+  if (T < 0 || d_local < 1 || d_local > kMaxWidth || ldx < d_local) return QKN_EINVAL;
+  if (T == 0) return QKN_OK;
+  if (!x || !slots_out || epoch == 0 || (reinterpret_cast<uintptr_t>(slots_out) & 7u))
+    return QKN_EINVAL;
+  HSeg s;
+  memset(&s, 0, sizeof(s));
+  s.x = x;
+  s.ldx = ldx;
+  s.d_local = d_local;
+  s.d_full = d_local;
+  const Span out{reinterpret_cast<uintptr_t>(slots_out), 1, T, T, 8};
+  int rc = check_overlaps(&s, 1, 1, 0, T, kPublish, kFormat[fmt].esz, &out, 1);
+  if (rc != QKN_OK) return rc;
+  WaitArgs wa;
+  memset(&wa, 0, sizeof(wa));
+  wa.slots[0] = slots_out;
+  wa.epoch = epoch;
+  wa.spin_limit = 1;
+  wa.co_resident = 1;
+  wa.group = 1;
+  return launch(&s, 1, 1, 0, T, 0.0f, kPublish, fmt, stream, &wa);
+}
+
+template <class S>
+int wait_impl(const S* segs_in, int nseg, int tp, int rank, int64_t T, float eps,
+              const qkn_wait* wait, int fmt, void* stream) {
+  if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
+  int rc = validate_common(T, eps, tp, rank);
+  if (rc != QKN_OK) return rc;
+  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  HSeg segs[2];
+  for (int i = 0; i < nseg; ++i) {
+    segs[i] = to_hseg(segs_in[i]);
+    if (seg_dims_bad(segs[i])) return QKN_EINVAL;
+  }
+  if (T == 0) return QKN_OK;
+  if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
+  Span extra[3];
+  int nextra = 0;
+  for (int i = 0; i < nseg; ++i) {
+    rc = check_seg_shape(segs[i], kFusedWait);
+    if (rc != QKN_OK) return rc;
+    if (segs[i].partials) return QKN_EINVAL;  // statistics travel in wait->slots
+    uint64_t* sl = wait->slots[i];
+    if (!sl || (reinterpret_cast<uintptr_t>(sl) & 7u)) return QKN_EINVAL;
+    extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
+  }
+  extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
+  rc = check_overlaps(segs, nseg, tp, rank, T, kFusedWait, kFormat[fmt].esz, extra, nextra);
+  if (rc != QKN_OK) return rc;
+  WaitArgs wa;
+  wa.slots[0] = wait->slots[0];
+  wa.slots[1] = nseg == 2 ? wait->slots[1] : nullptr;
+  wa.status = wait->status;
+  wa.spin_limit = wait->spin_limit;
+  wa.epoch = wait->epoch;
+  wa.co_resident = wait->co_resident;
+  wa.group = 1;
+  return launch(segs, nseg, tp, rank, T, eps, kFusedWait, fmt, stream, &wa);
+}
+
+template <class S>
+int group_impl(const S* segs_in, int nseg, int tp, int64_t T, float eps, const qkn_wait* wait,
+               int fmt, void* stream) {
+  if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
+  int rc = validate_common(T, eps, tp, 0);
+  if (rc != QKN_OK) return rc;
+  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  HSeg segs[2];
+  HSeg view[2];  // the full tensors, for shape and overlap checks
+  for (int i = 0; i < nseg; ++i) {
+    const HSeg s = to_hseg(segs_in[i]);
+    if (s.d_local < 1 || s.d_local > kMaxWidth || s.d_full != s.d_local * tp ||
+        s.ldx < s.d_full || s.ldy < s.d_full)
+      return QKN_EINVAL;
+    segs[i] = s;
+    view[i] = s;
+    view[i].d_local = s.d_full;
+    view[i].inv_rms = nullptr;
+  }
+  if (T == 0) return QKN_OK;
+  if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
+  Span extra[5];
+  int nextra = 0;
+  for (int i = 0; i < nseg; ++i) {
+    rc = check_seg_shape(view[i], kFusedWait);
+    if (rc != QKN_OK) return rc;
+    if (segs[i].partials) return QKN_EINVAL;
+    uint64_t* sl = wait->slots[i];
+    if (!sl || (reinterpret_cast<uintptr_t>(sl) & 7u)) return QKN_EINVAL;
+    extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
+    if (segs[i].inv_rms)
+      extra[nextra++] = Span{reinterpret_cast<uintptr_t>(segs[i].inv_rms), 1, tp * T, tp * T, 4};
+  }
+  extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
+  rc = check_overlaps(view, nseg, tp, 0, T, kFusedWait, kFormat[fmt].esz, extra, nextra);
+  if (rc != QKN_OK) return rc;
+  WaitArgs wa;
+  wa.slots[0] = wait->slots[0];
+  wa.slots[1] = nseg == 2 ? wait->slots[1] : nullptr;
+  wa.status = wait->status;
+  wa.spin_limit = wait->spin_limit;
+  wa.epoch = wait->epoch;
+  wa.co_resident = wait->co_resident;
+  wa.group = tp;
+  return launch(segs, nseg, tp, 0, T, eps, kFusedWait, fmt, stream, &wa);
+}
+
 }  // namespace
 
 namespace qkn_host {
@@ -1720,110 +1838,32 @@ int qkn_full_fp8(const qkn_seg8* segs, int nseg, int64_t T, float eps, void* str
 
 int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
                          uint64_t* slots_out, uint32_t epoch, void* stream) {
-  if (T < 0 || d_local < 1 || d_local > kMaxWidth || ldx < d_local) return QKN_EINVAL;
-  if (T == 0) return QKN_OK;
-  if (!x || !slots_out || epoch == 0 || (reinterpret_cast<uintptr_t>(slots_out) & 7u))
-    return QKN_EINVAL;
-  HSeg s;
-  memset(&s, 0, sizeof(s));
-  s.x = x;
-  s.ldx = ldx;
-  s.d_local = d_local;
-  s.d_full = d_local;
-  const Span out{reinterpret_cast<uintptr_t>(slots_out), 1, T, T, 8};
-  int rc = check_overlaps(&s, 1, 1, 0, T, kPublish, 2, &out, 1);
-  if (rc != QKN_OK) return rc;
-  WaitArgs wa;
-  memset(&wa, 0, sizeof(wa));
-  wa.slots[0] = slots_out;
-  wa.epoch = epoch;
-  wa.spin_limit = 1;
-  wa.co_resident = 1;
-  wa.group = 1;
-  return launch(&s, 1, 1, 0, T, 0.0f, kPublish, kBf16, stream, &wa);
+  return publish_impl(x, ldx, T, d_local, slots_out, epoch, kBf16, stream);
 }
 
-int qkn_fused_shard_wait(const qkn_seg* segs_in, int nseg, int tp, int rank, int64_t T, float eps,
-                         const qkn_wait* wait, void* stream) {
-  if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
-  int rc = validate_common(T, eps, tp, rank);
-  if (rc != QKN_OK) return rc;
-  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
-  HSeg segs[2];
-  for (int i = 0; i < nseg; ++i) {
-    segs[i] = to_hseg(segs_in[i]);
-    if (seg_dims_bad(segs[i])) return QKN_EINVAL;
-  }
-  if (T == 0) return QKN_OK;
-  if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
-  Span extra[3];
-  int nextra = 0;
-  for (int i = 0; i < nseg; ++i) {
-    rc = check_seg_shape(segs[i], kFusedWait);
-    if (rc != QKN_OK) return rc;
-    if (segs[i].partials) return QKN_EINVAL;  // statistics travel in wait->slots
-    uint64_t* sl = wait->slots[i];
-    if (!sl || (reinterpret_cast<uintptr_t>(sl) & 7u)) return QKN_EINVAL;
-    extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
-  }
-  extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
-  rc = check_overlaps(segs, nseg, tp, rank, T, kFusedWait, 2, extra, nextra);
-  if (rc != QKN_OK) return rc;
-  WaitArgs wa;
-  wa.slots[0] = wait->slots[0];
-  wa.slots[1] = nseg == 2 ? wait->slots[1] : nullptr;
-  wa.status = wait->status;
-  wa.spin_limit = wait->spin_limit;
-  wa.epoch = wait->epoch;
-  wa.co_resident = wait->co_resident;
-  wa.group = 1;
-  return launch(segs, nseg, tp, rank, T, eps, kFusedWait, kBf16, stream, &wa);
+int qkn_publish_partials_fp8(const uint8_t* x, int64_t ldx, int64_t T, int64_t d_local,
+                             uint64_t* slots_out, uint32_t epoch, void* stream) {
+  return publish_impl(x, ldx, T, d_local, slots_out, epoch, kFp8, stream);
 }
 
-int qkn_fused_group_wait(const qkn_seg* segs_in, int nseg, int tp, int64_t T, float eps,
+int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
                          const qkn_wait* wait, void* stream) {
-  if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
-  int rc = validate_common(T, eps, tp, 0);
-  if (rc != QKN_OK) return rc;
-  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
-  HSeg segs[2];
-  HSeg view[2];  // the full tensors, for shape and overlap checks
-  for (int i = 0; i < nseg; ++i) {
-    const HSeg s = to_hseg(segs_in[i]);
-    if (s.d_local < 1 || s.d_local > kMaxWidth || s.d_full != s.d_local * tp ||
-        s.ldx < s.d_full || s.ldy < s.d_full)
-      return QKN_EINVAL;
-    segs[i] = s;
-    view[i] = s;
-    view[i].d_local = s.d_full;
-    view[i].inv_rms = nullptr;
-  }
-  if (T == 0) return QKN_OK;
-  if (!wait->status || (reinterpret_cast<uintptr_t>(wait->status) & 3u)) return QKN_EINVAL;
-  Span extra[5];
-  int nextra = 0;
-  for (int i = 0; i < nseg; ++i) {
-    rc = check_seg_shape(view[i], kFusedWait);
-    if (rc != QKN_OK) return rc;
-    if (segs[i].partials) return QKN_EINVAL;
-    uint64_t* sl = wait->slots[i];
-    if (!sl || (reinterpret_cast<uintptr_t>(sl) & 7u)) return QKN_EINVAL;
-    extra[nextra++] = Span{reinterpret_cast<uintptr_t>(sl), 1, tp * T, tp * T, 8};
-    if (segs[i].inv_rms)
-      extra[nextra++] = Span{reinterpret_cast<uintptr_t>(segs[i].inv_rms), 1, tp * T, tp * T, 4};
-  }
-  extra[nextra++] = Span{reinterpret_cast<uintptr_t>(wait->status), 1, 1, 1, 4};
-  rc = check_overlaps(view, nseg, tp, 0, T, kFusedWait, 2, extra, nextra);
-  if (rc != QKN_OK) return rc;
-  WaitArgs wa;
-  wa.slots[0] = wait->slots[0];
-  wa.slots[1] = nseg == 2 ? wait->slots[1] : nullptr;
-  wa.status = wait->status;
-  wa.spin_limit = wait->spin_limit;
-  wa.epoch = wait->epoch;
-  wa.co_resident = wait->co_resident;
-  wa.group = tp;
-  return launch(segs, nseg, tp, 0, T, eps, kFusedWait, kBf16, stream, &wa);
+  return wait_impl(segs, nseg, tp, rank, T, eps, wait, kBf16, stream);
+}
+
+int qkn_fused_shard_wait_fp8(const qkn_seg8* segs, int nseg, int tp, int rank, int64_t T,
+                             float eps, const qkn_wait* wait, void* stream) {
+  return wait_impl(segs, nseg, tp, rank, T, eps, wait, kFp8, stream);
+}
+
+int qkn_fused_group_wait(const qkn_seg* segs, int nseg, int tp, int64_t T, float eps,
+                         const qkn_wait* wait, void* stream) {
+  return group_impl(segs, nseg, tp, T, eps, wait, kBf16, stream);
+}
+
+int qkn_fused_group_wait_fp8(const qkn_seg8* segs, int nseg, int tp, int64_t T, float eps,
+                             const qkn_wait* wait, void* stream) {
+  return group_impl(segs, nseg, tp, T, eps, wait, kFp8, stream);
 }
 
 const char* qkn_strerror(int status) {

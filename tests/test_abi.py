@@ -622,3 +622,28 @@ def test_calib_validation(dry):
     assert dry.qkn_calib_copy(X, X + (1 << 19), 1 << 20, 2048, None) == L.QKN_EOVERLAP
     assert dry.qkn_calib_empty(None) == 0
     assert L.qkn_last_launch()["kernel"] == "calib_empty"
+
+
+def test_fp8_wait_entries(dry):
+    # FP8 rows of 1024 codes: one 16-byte chunk per lane
+    q = _seg(BASE, 1024, BASE + 64 * MB, None, BASE + 128 * MB, 1024, 1024, 4096)
+    k = _seg(BASE + 256 * MB, 256, BASE + 300 * MB, None, BASE + 400 * MB, 256, 256, 1024)
+    arr = (L.QknSeg * 2)(q, k)
+    w = _wait_block()
+    assert dry.qkn_fused_shard_wait_fp8(arr, 2, 4, 1, 64, ctypes.c_float(1e-6), ctypes.byref(w),
+                                        None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_pa2_fp8<1,1>/fused_wait"
+    assert dry.qkn_publish_partials_fp8(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_fp8<1,0>/publish"
+    full = (L.QknSeg * 1)(_seg(BASE, 4096, BASE + 64 * MB, None, BASE + 128 * MB, 4096, 1024, 4096))
+    assert dry.qkn_fused_group_wait_fp8(full, 1, 4, 64, ctypes.c_float(1e-6), ctypes.byref(w),
+                                        None) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_pa2_fp8<1,0>/fused_wait"
+    # the register path's limits are in bytes: 8 codes per row are not a 16-byte chunk
+    odd = (L.QknSeg * 1)(_seg(BASE, 1032, BASE + 64 * MB, None, BASE + 128 * MB, 1032, 1032, 4128))
+    assert dry.qkn_fused_shard_wait_fp8(odd, 1, 4, 1, 64, ctypes.c_float(1e-6), ctypes.byref(w),
+                                        None) == L.QKN_ENOTSUP
+    # validation as for bf16
+    assert dry.qkn_publish_partials_fp8(BASE, 1024, 64, 1024, BASE + 512 * MB, 0, None) == L.QKN_EINVAL
+    assert dry.qkn_fused_shard_wait_fp8(arr, 2, 4, 1, 64, ctypes.c_float(1e-6), None, None) == \
+        L.QKN_EINVAL

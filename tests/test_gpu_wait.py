@@ -19,7 +19,7 @@ import torch
 import workloads
 from paper_2608_09160_amd import _lib as L
 
-from gpu_util import DEV, bits_of, inputs, run_fused_rank, to_dev_bf16, to_dev_f32
+from gpu_util import DEV, bits_of, inputs, run_fused_rank, to_dev_act, to_dev_f32
 
 pytestmark = pytest.mark.gpu
 
@@ -30,9 +30,9 @@ def _rank_inputs(wl, data, rank):
     segs, peers = [], []
     for key, gkey, d_full in (("xq", "gq", wl.q_full), ("xk", "gk", wl.k_full)):
         cols = workloads.shard_cols(d_full, wl.tp, rank)
-        segs.append(L.Seg(x=to_dev_bf16(data[key][:, cols]), w=to_dev_f32(data[gkey][cols]),
+        segs.append(L.Seg(x=to_dev_act(data[key][:, cols]), w=to_dev_f32(data[gkey][cols]),
                           d_full=d_full, inv_rms=torch.empty(wl.T, dtype=torch.float32, device=DEV)))
-        peers.append([to_dev_bf16(data[key][:, workloads.shard_cols(d_full, wl.tp, k)])
+        peers.append([to_dev_act(data[key][:, workloads.shard_cols(d_full, wl.tp, k)])
                       for k in range(wl.tp)])
     return segs, peers
 
@@ -48,12 +48,13 @@ def _check_against_fused(wl, data, rank, segs):
         assert np.array_equal(s.inv_rms.cpu().numpy(), ref[t]["inv"]), (rank, t)
 
 
-def test_producers_and_consumer_on_separate_streams():
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_producers_and_consumer_on_separate_streams(dtype):
     """Peers publish from another stream; the consumer uses whatever it finds,
     waiting where a slot is not there yet. (Kernels on separate streams are not
     guaranteed to run at the same time on one GPU, so the producers are issued
     first: the consumer may or may not have to wait, and must be right either way.)"""
-    wl = workloads.DECODE_TP4
+    wl = workloads.DECODE_TP4.with_dtype(dtype) if dtype == "fp8" else workloads.DECODE_TP4
     data = inputs(wl)
     rank = 1
     segs, peers = _rank_inputs(wl, data, rank)
@@ -77,7 +78,8 @@ def test_producers_and_consumer_on_separate_streams():
     # the own slots were published with the epoch and the Phase A value
     own = slots[0][rank].cpu().numpy().view(np.uint64)
     assert np.all((own >> np.uint64(32)) == 1)
-    alone = L.qkn_partial_sumsq(peers[0][rank]).cpu().numpy()
+    partial = L.qkn_partial_sumsq_fp8 if dtype == "fp8" else L.qkn_partial_sumsq
+    alone = partial(peers[0][rank]).cpu().numpy()
     assert np.array_equal((own & np.uint64(0xFFFFFFFF)).astype(np.uint32).view(np.float32), alone)
 
 
@@ -93,6 +95,15 @@ def test_whole_group_in_one_launch(wl):
     Default schedule: each token's statistics published two tokens ahead."""
     info = _run_group_and_check(wl)
     assert info["kernel"].startswith("rows_pa2<"), info
+
+
+@pytest.mark.parametrize("wl", [workloads.DECODE_TP4.with_dtype("fp8"), workloads.DECODE_TP8.with_dtype("fp8"),
+                                workloads.PREFILL_TP2.with_tokens(2048).with_dtype("fp8")],
+                         ids=lambda w: w.name)
+def test_whole_group_in_one_launch_fp8(wl):
+    """FP8-E4M3 activations: the same bits as qkn_fused_shard_fp8 per rank."""
+    info = _run_group_and_check(wl)
+    assert info["kernel"].startswith("rows_pa2_fp8<"), info
 
 
 @pytest.mark.parametrize("sched", [0, 1, 2])
@@ -116,7 +127,7 @@ def _run_group_and_check(wl):
     data = inputs(wl)
     slots = _slot_arrays(wl)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
-    segs = [L.Seg(x=to_dev_bf16(data[key]), w=to_dev_f32(data[gkey]), d_full=d_full,
+    segs = [L.Seg(x=to_dev_act(data[key]), w=to_dev_f32(data[gkey]), d_full=d_full,
                   inv_rms=torch.empty((wl.tp, wl.T), dtype=torch.float32, device=DEV))
             for key, gkey, d_full in (("xq", "gq", wl.q_full), ("xk", "gk", wl.k_full))]
     torch.cuda.synchronize()
