@@ -647,3 +647,20 @@ def test_fp8_wait_entries(dry):
     assert dry.qkn_publish_partials_fp8(BASE, 1024, 64, 1024, BASE + 512 * MB, 0, None) == L.QKN_EINVAL
     assert dry.qkn_fused_shard_wait_fp8(arr, 2, 4, 1, 64, ctypes.c_float(1e-6), None, None) == \
         L.QKN_EINVAL
+
+
+def test_proj_size_limits(lib):
+    """Byte offsets of the projection's buffer descriptors are 32-bit: x of
+    2^31 bytes or more, or a weight slice that large, is not supported."""
+    X, W, Y, P, WS = BASE, BASE + (8 << 30), BASE + (16 << 30), BASE + (24 << 30), BASE + (25 << 30)
+    h = 4096
+    ok = _pseg(W, h, Y, 2048, P, 2048)
+    for T, expect in ((262143, 0), (262144, L.QKN_ENOTSUP)):  # T * 4096 * 2 bytes vs 2^31
+        need = lib.qkn_proj_workspace_bytes(T, h, (L.QknProjSeg * 1)(ok), 1)
+        if expect == 0:
+            assert dry_proj_ok(lib, X, h, T, h, [ok], WS, need)
+        else:
+            assert _proj(lib, X, h, T, h, [ok], WS, need) == expect
+    big = _pseg(W, h, Y, 262144, P, 262144)  # 262144 rows x 4096 x 2 bytes = 2^31
+    need = lib.qkn_proj_workspace_bytes(64, h, (L.QknProjSeg * 1)(big), 1)
+    assert _proj(lib, X, h, 64, h, [big], WS, need) == L.QKN_ENOTSUP
