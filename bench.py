@@ -49,6 +49,13 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--summarize", metavar="DIR",
                    help="write the profiles/ summaries from rocprofv3 CSV output in DIR and exit")
+    p.add_argument("--proj-only", action="store_true",
+                   help="run only the projection extra (Q/K projection with Phase A in its "
+                        "epilogue, and torch.mm of the same product) and print its JSON; "
+                        "the command profiled for profiles/counters_proj_*.txt")
+    p.add_argument("--summarize-proj", metavar="DIR",
+                   help="write profiles/counters_proj_*.txt from rocprofv3 --pmc CSV output of "
+                        "`bench.py --proj-only` in DIR/pmc_proj1 and DIR/pmc_proj2")
     p.add_argument("--calibration-copy", action="store_true",
                    help="also run a plain device copy of Q's input (known bytes) a few times, "
                         "to scale profiler byte counters")
@@ -468,6 +475,53 @@ def proj_extra(torch, L, workloads, wl, rank, steps=50):
             "torch_mm_tflops": round(flops / (tm * 1e-3) / 1e12, 1)}
 
 
+PROJ_COUNTERS = (
+    ("pmc_proj1", "SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_LDS "
+                  "SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_INSTS_MFMA"),
+    ("pmc_proj2", "GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_ACTIVE_INST_LDS"),
+)
+
+
+def summarize_proj(outdir: str) -> None:
+    """Counters of the projection kernel and of torch.mm (hipBLASLt) of the same
+    product, from two rocprofv3 --pmc runs of `bench.py --proj-only`, into
+    profiles/counters_proj_prefill_T8192_h4096_q2048_k512.txt (means per
+    dispatch)."""
+    import csv
+    import collections
+    cmds, rows = [], collections.defaultdict(lambda: collections.defaultdict(list))
+    for sub, counters in PROJ_COUNTERS:
+        path = os.path.join(outdir, sub)
+        files = [f for f in os.listdir(path) if f.endswith("counter_collection.csv")]
+        if not files:
+            raise SystemExit(f"no counter CSV in {path}")
+        cmds.append(f"rocprofv3 --pmc {counters} --output-format csv -d gpurun_out/{sub} -o p "
+                    "-- python -u bench.py --proj-only")
+        for r in csv.DictReader(open(os.path.join(path, files[0]))):
+            name = r["Kernel_Name"]
+            if "qkn_proj_gemm" in name:
+                key = "qkn_proj_gemm_dl (this library)"
+            elif name.startswith("Cijk"):
+                key = "hipBLASLt GEMM (torch.mm)"
+            else:
+                continue
+            rows[key][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    lines = ["Q/K projection, 8192 tokens x hidden 4096 -> 2048 + 512 columns (bf16, fp32 accumulation)",
+             "commands (on the MI355X, from the repository root):"]
+    lines += ["  " + c for c in cmds]
+    lines += ["  python bench.py --summarize-proj gpurun_out",
+              "mean counter value per dispatch (sums over the GPU):"]
+    for key in sorted(rows):
+        lines.append(key + ":")
+        for c in sorted(rows[key]):
+            v = rows[key][c]
+            lines.append(f"  {c}: {sum(v) / len(v):.0f}")
+    out = os.path.join(ROOT, "profiles", "counters_proj_prefill_T8192_h4096_q2048_k512.txt")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def cpu_baseline(wl, rank, data, seconds):
     """The fp64 oracle as it stands, on the host: bounded sample of the workload."""
     from oracle import qknorm as Q
@@ -499,6 +553,9 @@ def main():
     if args.summarize:
         summarize(args.summarize)
         return 0
+    if args.summarize_proj:
+        summarize_proj(args.summarize_proj)
+        return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU's share of the sharded QK-Norm; the peer ranks "
@@ -515,6 +572,10 @@ def main():
         return 1
     L.load()
     wl = workloads.WORKLOADS[args.workload]
+    if args.proj_only:
+        out = {"proj_partial_prefill": proj_extra(torch, L, workloads, wl, args.rank, steps=10)}
+        print(json.dumps(out), flush=True)
+        return 0
     data = workloads.generate(wl)
     min_fp = args.min_footprint_mb << 20
 
