@@ -321,7 +321,7 @@ def trace_name(launch_name: str) -> str:
     """Profiler (demangled) name of the kernel a launch name denotes, e.g.
     "rows<4,1>/fused" -> "void qkn_rows<FmtBf16, 4, 1, 0, 0>"."""
     import re
-    m = re.fullmatch(r"(rows|rows_pf|rows_pa|rows_pa2|rows_fp8|wide|wide_fp8)<(\d+),(\d+)>/(\w+)", launch_name)
+    m = re.fullmatch(r"(rows|rows_pf|rows_pa|rows_pa2|rows_pa3|rows_fp8|wide|wide_fp8)<(\d+),(\d+)>/(\w+)", launch_name)
     if not m:
         raise ValueError(f"no profiler name for {launch_name!r}")
     fam, n0, n1, mode = m.groups()
@@ -329,7 +329,7 @@ def trace_name(launch_name: str) -> str:
     mode_id = ["fused", "apply", "partial", "fused_wait", "publish"].index(mode)
     if fam.startswith("wide"):
         return f"void qkn_wide<{fmt}, {n0}, {n1}, {mode_id}>"
-    sched = {"rows_pf": 1, "rows_pa": 2, "rows_pa2": 3}.get(fam, 0)
+    sched = {"rows_pf": 1, "rows_pa": 2, "rows_pa2": 3, "rows_pa3": 4}.get(fam, 0)
     return f"void qkn_rows<{fmt}, {n0}, {n1}, {mode_id}, {sched}>"
 
 

@@ -793,90 +793,65 @@ __global__ __launch_bounds__(256) void qkn_rows(const KParams p) {
   CursorBytes nb;
   make_cursors<F, MODE>(p, ws, t, step, c, dc, nb);
   TokenRegs<N0, M1> ra;
-  if constexpr (SCHED == 2) {
-    static_assert(MODE == kFusedWait, "the publish-ahead schedule is a wait-mode schedule");
-    // Publish ahead: a token's statistics are published one token before it
-    // waits for the other ranks' (its rows requested two tokens before), so
-    // that by the time a wavefront polls, its peers -- which run the same
-    // schedule -- have usually published long since. Step with token X
-    // current, Y next and Z the one after: issue X's first poll, request Z's
-    // rows (after the poll, so that waiting for the poll, which the in-order
-    // memory counter measures, does not wait for Z), publish Y, then wait for
-    // X's peers and finish X. Three register
-    // sets take the three roles in turn (the loop is unrolled by three, so no
-    // copy waits on requests in flight). Waits still move only to tokens
-    // whose peers published before waiting themselves, so with every
-    // wavefront resident no chain of waits can close.
-    TokenRegs<N0, M1> rb, rcc;
+  if constexpr (SCHED >= 2) {
+    static_assert(MODE == kFusedWait, "the publish-ahead schedules are wait-mode schedules");
+    // Publish ahead by D = SCHED - 1 tokens: a token's statistics are published
+    // D tokens before it waits for the other ranks' (its rows requested D + 1
+    // tokens before), so that by the time a wavefront polls, its peers --
+    // which run the same schedule -- have usually published long since. A
+    // step, with token X current: issue X's first poll, request the rows of
+    // token X + D + 1 (after the poll, so that waiting for the poll, which the
+    // in-order memory counter measures, does not wait for those rows), publish
+    // token X + D, then wait for X's peers and finish X. D + 2 register sets
+    // take the roles in turn (the steps are unrolled D + 2 at a time, so every
+    // index is a constant and no copy waits on requests in flight). Waits move
+    // only to tokens whose peers published them before waiting on anything
+    // later, so with every wavefront resident no chain of waits can close.
+    constexpr int D = SCHED - 1;
+    constexpr int NS = D + 2;
+    TokenRegs<N0, M1> r[NS];
+    Cursor cur[NS];
+    float o0[NS], o1[NS];
     const int64_t last = end - 1;
-    fetch_token<F, N0, N1, MODE, false>(p, c, nb, lane, own_rank, ra);
-    Cursor cb = c, cc = c;
-    advance(cb, dc);
-    fetch_token<F, N0, N1, MODE, false>(p, cb, nb, lane, own_rank, rb, t + step <= last);
-    float oa0 = 0.0f, oa1 = 0.0f, ob0 = 0.0f, ob1 = 0.0f, oc0 = 0.0f, oc1 = 0.0f;
-    publish_token<F, N0, N1>(p, c, lane, ra, oa0, oa1);
-#define QKN_PA_STEP(cx, rx, ox0, ox1, cy, ry, oy0, oy1, cz, rz)                                 \
-  {                                                                                             \
-    const bool live_y = t + step <= last;                                                       \
-    const uint64_t w0_ = poll_slots_at(cx.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, true);    \
-    uint64_t w1_ = 0;                                                                           \
-    if constexpr (N1 > 0) w1_ = poll_slots_at(cx.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, true); \
-    cz = cy;                                                                                    \
-    advance(cz, dc);                                                                            \
-    fetch_token<F, N0, N1, MODE, false>(p, cz, nb, lane, own_rank, rz, t + 2 * step <= last);   \
-    if (live_y) publish_token<F, N0, N1>(p, cy, lane, ry, oy0, oy1);                            \
-    finish_waiting_token<F, N0, N1>(p, cx, nb, lane, own_rank, g0, g1, rx, ox0, ox1, w0_, w1_,  \
-                                    given_up);                                                  \
-    if (!live_y) break;                                                                         \
-    t += step;                                                                                  \
-  }
-    while (true) {
-      QKN_PA_STEP(c, ra, oa0, oa1, cb, rb, ob0, ob1, cc, rcc)
-      QKN_PA_STEP(cb, rb, ob0, ob1, cc, rcc, oc0, oc1, c, ra)
-      QKN_PA_STEP(cc, rcc, oc0, oc1, c, ra, oa0, oa1, cb, rb)
+    cur[0] = c;
+#pragma unroll
+    for (int k = 1; k <= D; ++k) {
+      cur[k] = cur[k - 1];
+      advance(cur[k], dc);
     }
-#undef QKN_PA_STEP
-    return;
-  } else if constexpr (SCHED == 3) {
-    static_assert(MODE == kFusedWait, "the publish-ahead schedule is a wait-mode schedule");
-    // Publish two ahead: as above with four tokens in registers -- X waits and
-    // is finished, Y was published a step ago, Z is published now, W's rows
-    // are requested -- so a peer may lag two tokens before anyone waits.
-    TokenRegs<N0, M1> rb, rcc, rd;
-    const int64_t last = end - 1;
-    fetch_token<F, N0, N1, MODE, false>(p, c, nb, lane, own_rank, ra);
-    Cursor cb = c, cc = c, cd = c;
-    advance(cb, dc);
-    fetch_token<F, N0, N1, MODE, false>(p, cb, nb, lane, own_rank, rb, t + step <= last);
-    cc = cb;
-    advance(cc, dc);
-    fetch_token<F, N0, N1, MODE, false>(p, cc, nb, lane, own_rank, rcc, t + 2 * step <= last);
-    float oa0 = 0.0f, oa1 = 0.0f, ob0 = 0.0f, ob1 = 0.0f, oc0 = 0.0f, oc1 = 0.0f, od0 = 0.0f,
-          od1 = 0.0f;
-    publish_token<F, N0, N1>(p, c, lane, ra, oa0, oa1);
-    if (t + step <= last) publish_token<F, N0, N1>(p, cb, lane, rb, ob0, ob1);
-#define QKN_PA2_STEP(cx, rx, ox0, ox1, cy, ry, cz, rz, oz0, oz1, cw, rw)                         \
-  {                                                                                             \
-    const bool live_y = t + step <= last;                                                       \
-    const uint64_t w0_ = poll_slots_at(cx.sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, true);    \
-    uint64_t w1_ = 0;                                                                           \
-    if constexpr (N1 > 0) w1_ = poll_slots_at(cx.sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, true); \
-    cw = cz;                                                                                    \
-    advance(cw, dc);                                                                            \
-    fetch_token<F, N0, N1, MODE, false>(p, cw, nb, lane, own_rank, rw, t + 3 * step <= last);   \
-    if (t + 2 * step <= last) publish_token<F, N0, N1>(p, cz, lane, rz, oz0, oz1);              \
-    finish_waiting_token<F, N0, N1>(p, cx, nb, lane, own_rank, g0, g1, rx, ox0, ox1, w0_, w1_,  \
-                                    given_up);                                                  \
-    if (!live_y) break;                                                                         \
-    t += step;                                                                                  \
-  }
-    while (true) {
-      QKN_PA2_STEP(c, ra, oa0, oa1, cb, rb, cc, rcc, oc0, oc1, cd, rd)
-      QKN_PA2_STEP(cb, rb, ob0, ob1, cc, rcc, cd, rd, od0, od1, c, ra)
-      QKN_PA2_STEP(cc, rcc, oc0, oc1, cd, rd, c, ra, oa0, oa1, cb, rb)
-      QKN_PA2_STEP(cd, rd, od0, od1, c, ra, cb, rb, ob0, ob1, cc, rcc)
+#pragma unroll
+    for (int k = 0; k <= D; ++k)
+      fetch_token<F, N0, N1, MODE, false>(p, cur[k], nb, lane, own_rank, r[k],
+                                          t + k * step <= last);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) o0[k] = o1[k] = 0.0f;
+#pragma unroll
+    for (int k = 0; k < D; ++k)
+      if (t + k * step <= last) publish_token<F, N0, N1>(p, cur[k], lane, r[k], o0[k], o1[k]);
+    bool more = true;
+    while (more) {
+#pragma unroll
+      for (int k = 0; k < NS; ++k) {
+        const int x = k, z = (k + D) % NS, w = (k + D + 1) % NS;
+        const uint64_t w0 =
+            poll_slots_at(cur[x].sl[0], nb.sl[0], p.T, lane, p.tp, own_rank, true);
+        uint64_t w1 = 0;
+        if constexpr (N1 > 0)
+          w1 = poll_slots_at(cur[x].sl[1], nb.sl[1], p.T, lane, p.tp, own_rank, true);
+        cur[w] = cur[z];
+        advance(cur[w], dc);
+        fetch_token<F, N0, N1, MODE, false>(p, cur[w], nb, lane, own_rank, r[w],
+                                            t + (D + 1) * step <= last);
+        if (t + D * step <= last) publish_token<F, N0, N1>(p, cur[z], lane, r[z], o0[z], o1[z]);
+        finish_waiting_token<F, N0, N1>(p, cur[x], nb, lane, own_rank, g0, g1, r[x], o0[x],
+                                        o1[x], w0, w1, given_up);
+        if (t + step > last) {
+          more = false;
+          break;
+        }
+        t += step;
+      }
     }
-#undef QKN_PA2_STEP
     return;
   } else {
     fetch_token<F, N0, N1, MODE>(p, c, nb, lane, own_rank, ra);
@@ -1168,18 +1143,19 @@ const RowsFn kFusedTable[2][4][5] = {QKN_FULL_SET(FmtBf16, kFused, 0),
 const RowsFn kApplyTable[2][4] = {QKN_ONE_SET(FmtBf16, kApply, 0), QKN_ONE_SET(FmtBf16, kApply, 1)};
 const RowsFn kPartialTable[2][4] = {QKN_ONE_SET(FmtBf16, kPartial, 0),
                                     QKN_ONE_SET(FmtBf16, kPartial, 1)};
-// wait mode: 0 and 1 as above, 2 publish one token ahead, 3 two tokens ahead
-const RowsFn kFusedWaitTable[4][4][5] = {
+// wait mode: 0 and 1 as above, 2 + d - 1 publish d tokens ahead (d = 1, 2, 3)
+const RowsFn kFusedWaitTable[5][4][5] = {
     QKN_FULL_SET(FmtBf16, kFusedWait, 0), QKN_FULL_SET(FmtBf16, kFusedWait, 1),
-    QKN_FULL_SET(FmtBf16, kFusedWait, 2), QKN_FULL_SET(FmtBf16, kFusedWait, 3)};
+    QKN_FULL_SET(FmtBf16, kFusedWait, 2), QKN_FULL_SET(FmtBf16, kFusedWait, 3),
+    QKN_FULL_SET(FmtBf16, kFusedWait, 4)};
 const RowsFn kPublishTable[4] = QKN_ONE_SET(FmtBf16, kPublish, 0);
 // fp8: [N0 index][N1 index]; the wait modes with [schedule] first, as for bf16
 const RowsFn kFusedTable8[4][5] = QKN_FULL_SET8(kFused, 0);
 const RowsFn kApplyTable8[4] = QKN_ONE_SET8(kApply, 0);
 const RowsFn kPartialTable8[4] = QKN_ONE_SET8(kPartial, 0);
-const RowsFn kFusedWaitTable8[4][4][5] = {
+const RowsFn kFusedWaitTable8[5][4][5] = {
     QKN_FULL_SET8(kFusedWait, 0), QKN_FULL_SET8(kFusedWait, 1), QKN_FULL_SET8(kFusedWait, 2),
-    QKN_FULL_SET8(kFusedWait, 3)};
+    QKN_FULL_SET8(kFusedWait, 3), QKN_FULL_SET8(kFusedWait, 4)};
 const RowsFn kPublishTable8[4] = QKN_ONE_SET8(kPublish, 0);
 const GenericFn kGenericTable[2][3] = {
     {qkn_generic<FmtBf16, kFused>, qkn_generic<FmtBf16, kApply>, qkn_generic<FmtBf16, kPartial>},
@@ -1204,14 +1180,15 @@ const char* const kModeName[5] = {"fused", "apply", "partial", "fused_wait", "pu
 
 // Static names "rows<N0,N1>/mode" ("rows_pf<...>" when pipelined, "rows_fp8<...>" for fp8).
 const char* rows_name(int fmt, int mode, int sched, int i0, int i1) {
-  static char names[2][5][4][4][5][40];
+  static char names[2][5][5][4][5][40];
   static std::once_flag once;
   std::call_once(once, [] {
-    const char* const prefix[2][4] = {{"rows", "rows_pf", "rows_pa", "rows_pa2"},
-                                      {"rows_fp8", "rows_pf_fp8", "rows_pa_fp8", "rows_pa2_fp8"}};
+    const char* const prefix[2][5] = {
+        {"rows", "rows_pf", "rows_pa", "rows_pa2", "rows_pa3"},
+        {"rows_fp8", "rows_pf_fp8", "rows_pa_fp8", "rows_pa2_fp8", "rows_pa3_fp8"}};
     for (int fm = 0; fm < 2; ++fm)
       for (int m = 0; m < 5; ++m)
-        for (int f = 0; f < 4; ++f)
+        for (int f = 0; f < 5; ++f)
           for (int a = 0; a < 4; ++a)
             for (int b = 0; b < 5; ++b)
               snprintf(names[fm][m][f][a][b], sizeof(names[fm][m][f][a][b]), "%s<%d,%d>/%s",
@@ -1241,7 +1218,7 @@ const char* wide_name(int fmt, int mode, int i0, int i1) {
 
 // Options.
 int64_t g_opt_waves_per_cu = 0;
-int64_t g_opt_wait_schedule = 3;  // publish two tokens ahead
+int64_t g_opt_wait_schedule = 4;  // publish three tokens ahead
 int64_t g_opt_waves_per_block = 0;
 int64_t g_opt_force_generic = 0;
 int64_t g_opt_validate_only = 0;
@@ -1898,7 +1875,7 @@ int qkn_set_option(const char* key, int64_t value) {
     if (value != 0 && value != 1) return QKN_EINVAL;
     g_opt_prefetch = value;
   } else if (strcmp(key, "wait_schedule") == 0) {
-    if (value < 0 || value > 3) return QKN_EINVAL;
+    if (value < 0 || value > 4) return QKN_EINVAL;
     g_opt_wait_schedule = value;
   } else if (strcmp(key, "balance") == 0) {
     if (value != 0 && value != 1) return QKN_EINVAL;

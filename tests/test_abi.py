@@ -350,7 +350,7 @@ def _k_nopart():
 def test_wait_entry_validation(dry):
     ok = _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block())
     assert ok == 0
-    assert L.qkn_last_launch()["kernel"] == "rows_pa2<2,1>/fused_wait"  # publish two ahead
+    assert L.qkn_last_launch()["kernel"] == "rows_pa3<2,1>/fused_wait"  # publish three ahead
     for kw in (dict(epoch=0), dict(spin_limit=0), dict(co_resident=0), dict(status=None),
                dict(status=BASE + 700 * MB + 2), dict(slots=(None, BASE + 600 * MB)),
                dict(slots=(BASE + 512 * MB + 4, BASE + 600 * MB))):
@@ -373,17 +373,18 @@ def test_wait_entry_validation(dry):
 
 def test_wait_schedule_option(dry):
     try:
-        for sched, prefix in ((0, "rows"), (1, "rows_pf"), (2, "rows_pa"), (3, "rows_pa2")):
+        for sched, prefix in ((0, "rows"), (1, "rows_pf"), (2, "rows_pa"), (3, "rows_pa2"),
+                              (4, "rows_pa3")):
             assert dry.qkn_set_option(b"wait_schedule", sched) == 0
             assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block()) == 0
             assert L.qkn_last_launch()["kernel"] == f"{prefix}<2,1>/fused_wait"
         # the option does not touch the kernels without a wait
         assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
         assert L.qkn_last_launch()["kernel"] == "rows<2,1>/fused"
-        assert dry.qkn_set_option(b"wait_schedule", 4) == L.QKN_EINVAL
+        assert dry.qkn_set_option(b"wait_schedule", 5) == L.QKN_EINVAL
         assert dry.qkn_set_option(b"wait_schedule", -1) == L.QKN_EINVAL
     finally:
-        assert dry.qkn_set_option(b"wait_schedule", 3) == 0
+        assert dry.qkn_set_option(b"wait_schedule", 4) == 0
 
 
 def test_publish_entry_validation(dry):
@@ -409,7 +410,7 @@ def test_group_entry_validation(dry):
         return dry.qkn_fused_group_wait(arr, len(segs), tp, T, ctypes.c_float(1e-6),
                                         ctypes.byref(wait), None)
     assert call([full(1024, 4)], 4, _wait_block()) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows_pa2<2,0>/fused_wait"
+    assert L.qkn_last_launch()["kernel"] == "rows_pa3<2,0>/fused_wait"
     bad = full(1024, 4)
     bad.d_full = 4000
     assert call([bad], 4, _wait_block()) == L.QKN_EINVAL           # d_full != tp * d_local
@@ -632,13 +633,13 @@ def test_fp8_wait_entries(dry):
     w = _wait_block()
     assert dry.qkn_fused_shard_wait_fp8(arr, 2, 4, 1, 64, ctypes.c_float(1e-6), ctypes.byref(w),
                                         None) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows_pa2_fp8<1,1>/fused_wait"
+    assert L.qkn_last_launch()["kernel"] == "rows_pa3_fp8<1,1>/fused_wait"
     assert dry.qkn_publish_partials_fp8(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == 0
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<1,0>/publish"
     full = (L.QknSeg * 1)(_seg(BASE, 4096, BASE + 64 * MB, None, BASE + 128 * MB, 4096, 1024, 4096))
     assert dry.qkn_fused_group_wait_fp8(full, 1, 4, 64, ctypes.c_float(1e-6), ctypes.byref(w),
                                         None) == 0
-    assert L.qkn_last_launch()["kernel"] == "rows_pa2_fp8<1,0>/fused_wait"
+    assert L.qkn_last_launch()["kernel"] == "rows_pa3_fp8<1,0>/fused_wait"
     # the register path's limits are in bytes: 8 codes per row are not a 16-byte chunk
     odd = (L.QknSeg * 1)(_seg(BASE, 1032, BASE + 64 * MB, None, BASE + 128 * MB, 1032, 1032, 4128))
     assert dry.qkn_fused_shard_wait_fp8(odd, 1, 4, 1, 64, ctypes.c_float(1e-6), ctypes.byref(w),

@@ -92,9 +92,9 @@ GROUPS = [workloads.DECODE_TP4, workloads.DECODE_TP8, workloads.PREFILL_TP2.with
 def test_whole_group_in_one_launch(wl):
     """Every rank of the group in one launch: each wavefront publishes its rank's
     statistic and waits for the others'; all of them are resident at once.
-    Default schedule: each token's statistics published two tokens ahead."""
+    Default schedule: each token's statistics published three tokens ahead."""
     info = _run_group_and_check(wl)
-    assert info["kernel"].startswith("rows_pa2<"), info
+    assert info["kernel"].startswith("rows_pa3<"), info
 
 
 @pytest.mark.parametrize("wl", [workloads.DECODE_TP4.with_dtype("fp8"), workloads.DECODE_TP8.with_dtype("fp8"),
@@ -103,24 +103,24 @@ def test_whole_group_in_one_launch(wl):
 def test_whole_group_in_one_launch_fp8(wl):
     """FP8-E4M3 activations: the same bits as qkn_fused_shard_fp8 per rank."""
     info = _run_group_and_check(wl)
-    assert info["kernel"].startswith("rows_pa2_fp8<"), info
+    assert info["kernel"].startswith("rows_pa3_fp8<"), info
 
 
-@pytest.mark.parametrize("sched", [0, 1, 2])
+@pytest.mark.parametrize("sched", [0, 1, 2, 3])
 @pytest.mark.parametrize("wl", [workloads.DECODE_TP4, workloads.PREFILL_TP2.with_tokens(2048),
                                 workloads.Workload("tp3_T7_q384_k96", 7, 384, 96, 3, "normal", 9)],
                          ids=lambda w: w.name)
 def test_whole_group_other_schedules(wl, sched):
     """The same with the other schedules -- token by token (publish, then
     wait, per token; 1 also requests the next token early) and publishing one
-    token ahead -- identical results, also with fewer tokens than a schedule
-    keeps in flight."""
+    or two tokens ahead -- identical results, also with fewer tokens than a
+    schedule keeps in flight."""
     L.qkn_set_option("wait_schedule", sched)
     try:
         info = _run_group_and_check(wl)
-        assert info["kernel"].startswith(("rows<", "rows_pf<", "rows_pa<")[sched]), info
+        assert info["kernel"].startswith(("rows<", "rows_pf<", "rows_pa<", "rows_pa2<")[sched]), info
     finally:
-        L.qkn_set_option("wait_schedule", 3)
+        L.qkn_set_option("wait_schedule", 4)
 
 
 def _run_group_and_check(wl):
