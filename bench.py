@@ -284,13 +284,21 @@ def time_graph(torch, fn, per_graph, replays):
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_09160_amd", "csrc", "qkn.hip")
+# the row kernels' templates, their instantiation tables and the host code
+# that picks and launches them: counters taken before a change to any of these
+# no longer describe the kernel
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_09160_amd", "csrc", f)
+                  for f in ("qkn_kernels.h", "qkn_kern_rows.hip", "qkn_kern_wait.hip",
+                            "qkn_kern_wait8.hip", "qkn_kern_misc.hip", "qkn.hip")]
 
 
 def source_sha256() -> str:
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def counters_path(kernel: str, workload: str) -> str:
@@ -333,6 +341,14 @@ def trace_name(launch_name: str) -> str:
     return f"void qkn_rows<{fmt}, {n0}, {n1}, {mode_id}, {sched}>"
 
 
+def kernel_base_name(profiler_name: str) -> str:
+    """Profiler name without namespaces and parameter list, e.g.
+    "void qkn_dev::qkn_rows<qkn_dev::FmtBf16, 4, 1, 0, 0>(qkn_dev::KParams)"
+    -> "void qkn_rows<FmtBf16, 4, 1, 0, 0>"."""
+    return (profiler_name.replace("(anonymous namespace)::", "").replace("qkn_dev::", "")
+            .split("(")[0])
+
+
 def summarize(outdir: str) -> None:
     """Write the profile summaries of the headline kernel into profiles/ from
     rocprofv3 CSV output in `outdir`:
@@ -355,7 +371,7 @@ def summarize(outdir: str) -> None:
     rows = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Start_Timestamp"]))
     runs = []  # consecutive dispatches of one kernel and launch shape
     for r in rows:
-        name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+        name = kernel_base_name(r["Kernel_Name"])
         key = (name, int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
         d = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
         if runs and runs[-1][0] == key:
@@ -409,7 +425,7 @@ def summarize(outdir: str) -> None:
         f = glob.glob(os.path.join(outdir, sub, "*_counter_collection.csv"))[0]
         by = {}
         for r in csv.DictReader(open(f)):
-            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            name = kernel_base_name(r["Kernel_Name"])
             by.setdefault(name, []).append(float(r["Counter_Value"]))
         return by
     fetch, write = counter("pmc_fetch"), counter("pmc_write")

@@ -297,7 +297,8 @@ int qkn_last_launch(qkn_launch_info* info);
  *                    requested early, 2 = publish ahead: a token's
  *                    statistics are published one token before it waits for
  *                    the other ranks', 3 = two tokens before, 4 = three
- *                    tokens before (default); same results;
+ *                    tokens before (default; bf16 Q and K rows that are both
+ *                    wider than 2048 per rank take 1 instead); same results;
  *   "balance"        1 = shrink the grid so every wavefront takes the same
  *                    number of tokens, 0 = use the full grid (default);
  *   "token_blocks"   1 = each wavefront takes a contiguous range of tokens,

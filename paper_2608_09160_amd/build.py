@@ -15,7 +15,11 @@ import sys
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG_DIR)
-SOURCES = [os.path.join(PKG_DIR, "csrc", name) for name in ("qkn.hip", "qkn_proj.hip", "qkn_calib.hip")]
+# qkn_kern_*.hip instantiate the QK-Norm kernel tables (templates in
+# qkn_kernels.h), split so that the units compile in parallel.
+SOURCES = [os.path.join(PKG_DIR, "csrc", name)
+           for name in ("qkn.hip", "qkn_kern_rows.hip", "qkn_kern_wait.hip", "qkn_kern_wait8.hip",
+                        "qkn_kern_misc.hip", "qkn_proj.hip", "qkn_calib.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG_DIR, "libqkn.so")
 ARCH = "gfx950"
@@ -40,10 +44,21 @@ def _run(cmd):
 
 
 def build(asm: bool = False, verbose: bool = False) -> str:
-    """Compile libqkn.so (always recompiles). Returns the library path."""
+    """Compile libqkn.so (always recompiles): every source to an object in
+    parallel, then one shared library. Returns the library path."""
+    from concurrent.futures import ThreadPoolExecutor
+    objdir = os.path.join(PKG_DIR, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    objs = [os.path.join(objdir, os.path.splitext(os.path.basename(src))[0] + ".o")
+            for src in SOURCES]
+    jobs = max(1, min(len(SOURCES), os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(jobs) as pool:
+        outs = list(pool.map(lambda so: _run([HIPCC, *COMMON, "-fPIC", "-c", "-o", so[1], so[0]]),
+                             zip(SOURCES, objs)))
     tmp = LIB + ".tmp"
-    out = _run([HIPCC, *COMMON, "-shared", "-fPIC", "-o", tmp, *SOURCES])
+    outs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]))
     os.replace(tmp, LIB)
+    out = "\n".join(o for o in outs if o.strip())
     if verbose and out.strip():
         print(out)
     if asm:

@@ -665,3 +665,13 @@ def test_proj_size_limits(lib):
     big = _pseg(W, h, Y, 262144, P, 262144)  # 262144 rows x 4096 x 2 bytes = 2^31
     need = lib.qkn_proj_workspace_bytes(64, h, (L.QknProjSeg * 1)(big), 1)
     assert _proj(lib, X, h, 64, h, [big], WS, need) == L.QKN_ENOTSUP
+
+
+def test_wait_schedule_capped_for_the_widest_rows(dry):
+    q = _seg(BASE, 4096, BASE + 64 * MB, None, BASE + 128 * MB, 4096, 4096, 8192)
+    k = _seg(BASE + 256 * MB, 4096, BASE + 300 * MB, None, BASE + 400 * MB, 4096, 4096, 8192)
+    assert _fused_wait(dry, [q, k], 2, 1, 64, _wait_block()) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_pf<8,8>/fused_wait"
+    k2 = _seg(BASE + 256 * MB, 2048, BASE + 300 * MB, None, BASE + 400 * MB, 2048, 2048, 4096)
+    assert _fused_wait(dry, [q, k2], 2, 1, 64, _wait_block()) == 0
+    assert L.qkn_last_launch()["kernel"] == "rows_pa3<8,4>/fused_wait"
