@@ -63,8 +63,12 @@ def test_fused_every_rank_matches_oracle(wl):
     # concatenated shards == unsharded Eq. 1
     full = Q.qknorm_layerwise(data["xq"], data["xk"], data["gq"], data["gk"], 1, 0, wl.eps)
     for t in "qk":
-        compare.check_close(Q.decode_bf16(np.concatenate(ys[t], axis=1)), full[t]["y"],
-                            compare.OUTPUT_RTOL, f"{wl.name} {t} concat")
+        got = Q.decode_bf16(np.concatenate(ys[t], axis=1))
+        compare.check_close(got, full[t]["y"], compare.OUTPUT_RTOL, f"{wl.name} {t} concat")
+        # the three error metrics of Sec. IV-C against the fp64 output
+        m = compare.paper_error_metrics(got, full[t]["y"])
+        print(f"[parity] {wl.name} {t} max/mean/rms abs error "
+              f"{m['max_abs']:.3e} {m['mean_abs']:.3e} {m['rms_abs']:.3e}", flush=True)
 
 
 @pytest.mark.parametrize("wl", [workloads.TINY_FULL, workloads.PREFILL_TP2.with_tp(1).with_tokens(513)],
