@@ -475,9 +475,9 @@ def proj_extra(torch, L, workloads, wl, rank, steps=50):
     prep = L.PreparedProj(x, [L.ProjSeg(w=wq), L.ProjSeg(w=wk)])
     wqk_t = torch.cat([wq, wk]).t().contiguous()
     ours, lib = [], []
-    for _ in range(3):  # alternate, median of three regions each
-        ours.append(time_region(torch, lambda i: prep(), steps, 5) / steps)
-        lib.append(time_region(torch, lambda i: torch.mm(x, wqk_t), steps, 5) / steps)
+    for _ in range(5):  # alternate, median of five regions each
+        ours.append(time_region(torch, lambda i: prep(), steps, 10) / steps)
+        lib.append(time_region(torch, lambda i: torch.mm(x, wqk_t), steps, 10) / steps)
     prep()
     info = L.qkn_last_launch()
     t, tm = float(np.median(ours)), float(np.median(lib))

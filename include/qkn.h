@@ -308,8 +308,10 @@ int qkn_last_launch(qkn_launch_info* info);
  *   "force_generic"  1 = always take the general path (same results);
  *   "proj_tile"      qkn_proj_partial's kernel: 0 = automatic (split k for
  *                    decode-sized launches, else kernel 1), 1 = direct-to-
- *                    LDS two-stage kernel, never split, 2 = register-staged
- *                    kernel, never split (same results as 1);
+ *                    LDS two-stage kernel on 16 x 16 x 32 MFMAs, never split,
+ *                    2 = register-staged kernel, never split, 3 = direct-to-
+ *                    LDS kernel on 32 x 32 x 16 MFMAs, never split (2 and 3
+ *                    give the same results as 1);
  *   "validate_only"  1 = entry points validate their arguments and choose a
  *                    kernel (reported by qkn_last_launch, grid 0) but make no
  *                    HIP call and launch nothing.

@@ -6,14 +6,19 @@
 // Sec. III-A / Alg. 1), taken from the output tile while it is on chip.
 //
 // Kernel design (gfx950):
-//   * The contraction runs on the matrix cores: v_mfma_f32_32x32x16_bf16,
-//     fp32 accumulation. Both operands are k-contiguous (x is [T, hidden],
-//     W is [d_local, hidden]), so one 16-byte vector of 8 k-values is exactly
-//     one lane's A or B operand: lane l holds row (l mod 32), k-values
-//     8*(l/32) .. 8*(l/32)+7 of a 32 x 16 slab; the 32x32 result block leaves
-//     column (l mod 32), rows 8*(r/4) + 4*(l/32) + (r mod 4) in accumulator r.
+//   * The contraction runs on the matrix cores, fp32 accumulation. Both
+//     operands are k-contiguous (x is [T, hidden], W is [d_local, hidden]),
+//     so one 16-byte vector of 8 k-values is exactly one lane's A or B
+//     operand. Whole tiles use v_mfma_f32_16x16x32_bf16: lane l holds row
+//     (l mod 16), k-values 8*(l/16) .. 8*(l/16)+7 of a 16 x 32 slab, and the
+//     16x16 result block leaves column (l mod 16), rows 4*(l/16) + r in
+//     accumulator r. The split-k kernels (and a selectable whole-tile one) use
+//     v_mfma_f32_32x32x16_bf16: row (l mod 32), k-values 8*(l/32) .. +7 of a
+//     32 x 16 slab; result column (l mod 32), rows 8*(r/4) + 4*(l/32) +
+//     (r mod 4) in accumulator r. Both sum the same k-blocks of 16 in the same
+//     order per output (measured: bit-identical results).
 //   * A 256-thread workgroup owns a 128 x 128 output tile (four wavefronts in
-//     2 x 2, 64 x 64 each = 2 x 2 MFMA blocks); k advances 64 at a time
+//     2 x 2, 64 x 64 each = 4 x 4 or 2 x 2 MFMA blocks); k advances 64 at a time
 //     through two LDS stages that global memory fills directly (buffer_load
 //     ... lds, no VGPR staging): the loads of stage kt + 1 are in flight while
 //     stage kt is computed, one barrier per stage. Instead of padding, each
@@ -21,7 +26,8 @@
 //     group reads land on 16 distinct bank groups. Two such workgroups (64 KB
 //     of LDS each) share a CU. (Measured on MI355X against register-staged
 //     double buffering, three- and four-stage rings, k of 32 and 128 per stage
-//     and 256-wide tiles: this shape was the fastest.)
+//     and 256-wide tiles: this shape was the fastest; 16 x 16 x 32 MFMAs beat
+//     32 x 32 x 16 ones by 4-9 %.)
 //   * Global loads are raw buffer loads whose descriptors end at the last
 //     valid row, so rows past T or d_local read zeros; the k tail (hidden not
 //     a multiple of 64) is masked by moving the offset out of range.
@@ -156,6 +162,11 @@ __device__ __forceinline__ bool tile_of(int bid, int grid, int m_tiles, const Pr
 // bf16, stage the tile in LDS (`lds`, at least BM x OUT_ROW bf16; the caller
 // has finished with it), write it to y with coalesced 16-byte stores, and
 // take the Phase A statistic of each row's 128-column chunks.
+template <int BM, int BN, int OUT_ROW>
+__device__ __forceinline__ void epilogue_staged(const ProjParams& p, const ProjSegDev& s,
+                                                const uint16_t* out, int64_t m0, int n0,
+                                                int rows_a, int rows_b);
+
 template <int WMB, int WNB, int OUT_ROW>
 __device__ __forceinline__ void epilogue(const ProjParams& p, const ProjSegDev& s,
                                          const f32x16 (&acc)[WMB][WNB], uint16_t* lds, int64_t m0,
@@ -180,6 +191,44 @@ __device__ __forceinline__ void epilogue(const ProjParams& p, const ProjSegDev& 
       }
     }
   __syncthreads();
+  epilogue_staged<BM, BN, OUT_ROW>(p, s, out, m0, n0, rows_a, rows_b);
+}
+
+// The same for 16 x 16 MFMA blocks: a wavefront's (32 WMB) x 64 share of the
+// tile as (2 WMB) x 4 blocks; lane l holds column l mod 16 and rows
+// 4 (l / 16) .. 4 (l / 16) + 3 of each block.
+template <int WMB, int OUT_ROW>
+__device__ __forceinline__ void epilogue16(const ProjParams& p, const ProjSegDev& s,
+                                           const f32x4 (&acc)[2 * WMB][4], uint16_t* lds,
+                                           int64_t m0, int n0, int rows_a, int rows_b) {
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  uint16_t* out = lds;  // [64 WMB][OUT_ROW]
+#pragma unroll
+  for (int i = 0; i < 2 * WMB; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = wn * 64 + j * 16 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; r += 2) {
+        const int row = wm * 32 * WMB + i * 16 + 4 * (lane >> 4) + r;
+        const uint32_t pk = pack_bf16x2(acc[i][j][r], acc[i][j][r + 1]);
+        out[row * OUT_ROW + col] = static_cast<uint16_t>(pk & 0xffffu);
+        out[(row + 1) * OUT_ROW + col] = static_cast<uint16_t>(pk >> 16);
+      }
+    }
+  __syncthreads();
+  epilogue_staged<64 * WMB, 128, OUT_ROW>(p, s, out, m0, n0, rows_a, rows_b);
+}
+
+// Stores and statistic of a tile staged in LDS as bf16 ([BM][OUT_ROW]).
+template <int BM, int BN, int OUT_ROW>
+__device__ __forceinline__ void epilogue_staged(const ProjParams& p, const ProjSegDev& s,
+                                                const uint16_t* out, int64_t m0, int n0,
+                                                int rows_a, int rows_b) {
+  const int tid = static_cast<int>(threadIdx.x);
 
   // coalesced 16-byte stores of the tile rows (columns past d_local skipped)
   const uint32_t y_bytes = static_cast<uint32_t>(rows_a * s.ldy * 2);
@@ -369,6 +418,21 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
 // per row, which puts the 16 rows read by a 16-lane group at 16 distinct
 // 16-byte bank groups. Lane l of a load instruction therefore fetches the
 // global k-vector that belongs at its fixed LDS slot.
+// Accumulators of a wavefront's (32 WMB) x 64 share of a tile: MI x MI MFMA
+// blocks, kM x kN of them, kR fp32 values per lane each.
+template <int MI, int WMB>
+struct AccOf;
+template <int WMB>
+struct AccOf<32, WMB> {
+  static constexpr int kM = WMB, kN = 2, kR = 16;
+  typedef f32x16 T[kM][kN];
+};
+template <int WMB>
+struct AccOf<16, WMB> {
+  static constexpr int kM = 2 * WMB, kN = 4, kR = 4;
+  typedef f32x4 T[kM][kN];
+};
+
 template <int WMB, int BK, int S>
 struct DlCfg {
   static constexpr int BM = 64 * WMB, BN = 128;        // tile rows (tokens), columns
@@ -419,11 +483,11 @@ __device__ __forceinline__ void vm_wait(int n) {
 // WMB x 2 MFMA blocks of 32 x 32; every accumulator takes its k-blocks of 16
 // in ascending order whatever the tile's height, so all tile shapes give the
 // same bits.
-template <int WMB, int BK, int S>
+template <int MI, int WMB, int BK, int S>
 __device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDev& s,
                                             unsigned char* lds, int64_t m0, int n0, int rows_a,
                                             int rows_b, int k_lo, int k_hi,
-                                            f32x16 (&acc)[WMB][2]) {
+                                            typename AccOf<MI, WMB>::T& acc) {
   using C = DlCfg<WMB, BK, S>;
   const int tid = static_cast<int>(threadIdx.x);
   const int lane = tid & 63;
@@ -468,20 +532,25 @@ __device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDe
     }                                                                                       \
   } while (0)
 
+  using A = AccOf<MI, WMB>;
 #pragma unroll
-  for (int i = 0; i < WMB; ++i)
+  for (int i = 0; i < A::kM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < A::kN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+      for (int r = 0; r < A::kR; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = (k_hi - k_lo + BK - 1) / BK;
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
     if (st < nk) QKN_ISSUE_STAGE(st, k_lo + st * BK);
 
-  const int frag_row = lane & 31;
-  const int frag_kv = lane >> 5;
+  // MI = 32: lane l supplies row (l mod 32) of a 32-row block and k-values
+  // 8 (l / 32) .. 8 (l / 32) + 7 of a 16-deep k-block; MI = 16: row (l mod 16)
+  // of a 16-row block and k-values 8 (l / 16) .. 8 (l / 16) + 7 of 32
+  const int frag_row = lane & (MI - 1);
+  const int frag_kv = lane / MI;
+  constexpr int kKBlock = 512 / MI;  // k per MFMA
   constexpr int kPerStage = C::kLoadsA + C::kLoadsB;  // load instructions per wave per stage
   for (int kt = 0; kt < nk; ++kt) {
     // stages kt + 1 .. kt + S - 2 may stay in flight
@@ -496,26 +565,30 @@ __device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDe
     const unsigned char* a = lds + (kt % S) * C::kStageBytes;
     const unsigned char* b = a + C::kTileBytesA;
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
+    for (int kk = 0; kk < BK; kk += kKBlock) {
       const int kv = kk / 8 + frag_kv;
-      bf16x8 af[WMB], bfr[2];
+      bf16x8 af[A::kM], bfr[A::kN];
 #pragma unroll
-      for (int i = 0; i < WMB; ++i) {
-        const int ra_row = wm * 32 * WMB + i * 32 + frag_row;
+      for (int i = 0; i < A::kM; ++i) {
+        const int ra_row = wm * 32 * WMB + i * MI + frag_row;
         af[i] = *reinterpret_cast<const bf16x8*>(
             a + ra_row * C::kRowBytes + ((kv ^ ((ra_row / C::kRowsPerGroup) % C::P)) * 16));
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int rb_row = wn * 64 + j * 32 + frag_row;
+      for (int j = 0; j < A::kN; ++j) {
+        const int rb_row = wn * 64 + j * MI + frag_row;
         bfr[j] = *reinterpret_cast<const bf16x8*>(
             b + rb_row * C::kRowBytes + ((kv ^ ((rb_row / C::kRowsPerGroup) % C::P)) * 16));
       }
 #pragma unroll
-      for (int i = 0; i < WMB; ++i)
+      for (int i = 0; i < A::kM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < A::kN; ++j) {
+          if constexpr (MI == 32)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
     }
   }
 #undef QKN_ISSUE_STAGE
@@ -530,6 +603,12 @@ struct TileAt {
 };
 template <int WMB>
 __device__ __forceinline__ TileAt tile_at(const ProjParams& p, int64_t row0, int mt, int nt) {
+  // The tile numbers are uniform, but the integer divisions that produced
+  // them run on the vector unit; without this the compiler can treat the
+  // buffer descriptors built from them as per-lane values and wrap every
+  // direct load in a loop over the lanes' descriptors.
+  mt = __builtin_amdgcn_readfirstlane(mt);
+  nt = __builtin_amdgcn_readfirstlane(nt);
   TileAt t;
   t.si = (p.nseg == 2 && nt >= p.seg[1].tile0) ? 1 : 0;
   const ProjSegDev& s = p.seg[t.si];
@@ -541,26 +620,30 @@ __device__ __forceinline__ TileAt tile_at(const ProjParams& p, int64_t row0, int
 }
 
 // One whole tile with its epilogue.
-template <int WMB, int BK, int S>
+template <int MI, int WMB, int BK, int S>
 __device__ __forceinline__ void dl_tile(const ProjParams& p, unsigned char* lds, int64_t row0,
                                         int mt, int nt) {
   const TileAt t = tile_at<WMB>(p, row0, mt, nt);
   const ProjSegDev& s = p.seg[t.si];
-  f32x16 acc[WMB][2];
-  dl_mainloop<WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, 0, p.hidden, acc);
+  typename AccOf<MI, WMB>::T acc;
+  dl_mainloop<MI, WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, 0, p.hidden, acc);
   __syncthreads();
-  epilogue<WMB, 2, DlCfg<WMB, BK, S>::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds), t.m0,
-                                               t.n0, t.rows_a, t.rows_b);
+  if constexpr (MI == 32)
+    epilogue<WMB, 2, DlCfg<WMB, BK, S>::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds),
+                                                 t.m0, t.n0, t.rows_a, t.rows_b);
+  else
+    epilogue16<WMB, DlCfg<WMB, BK, S>::kOutRow>(p, s, acc, reinterpret_cast<uint16_t*>(lds),
+                                                t.m0, t.n0, t.rows_a, t.rows_b);
 }
 
 // Whole 128 x 128 tiles, XCD-aware order.
-template <int BK, int S>
+template <int MI, int BK, int S>
 __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p) {
   __shared__ __align__(1024) unsigned char lds[DlCfg<2, BK, S>::kLdsBytes];
   int mt, nt;
   if (!tile_of(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), p.m_tiles, p, mt, nt))
     return;
-  dl_tile<2, BK, S>(p, lds, 0, mt, nt);
+  dl_tile<MI, 2, BK, S>(p, lds, 0, mt, nt);
 }
 
 // Split k: workgroup b takes k-slice b mod splits of tile b / splits (tiles
@@ -579,7 +662,7 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams
   const TileAt t = tile_at<WMB>(p, 0, mt, nt);
   const ProjSegDev& s = p.seg[t.si];
   f32x16 acc[WMB][2];
-  dl_mainloop<WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, k_lo, k_hi, acc);
+  dl_mainloop<32, WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, k_lo, k_hi, acc);
   // fp32 sums of this k-slice: lanes 0..31 of a row are 32 adjacent columns
   const int lane = static_cast<int>(threadIdx.x) & 63;
   const int wave = static_cast<int>(threadIdx.x) >> 6;
@@ -697,13 +780,16 @@ struct TileShape {
     qkn_proj_gemm<WM, WN, BK>, 64 * WM, 64 * WN, BK,                                     \
         static_cast<int>(TileCfg<WM, WN, BK>::kLds * sizeof(uint16_t)), NAME              \
   }
-#define QKN_DL(BK, S, NAME) \
-  TileShape { qkn_proj_gemm_dl<BK, S>, 128, 128, BK, DlCfg<2, BK, S>::kLdsBytes, NAME }
+#define QKN_DL(MI, BK, S, NAME) \
+  TileShape { qkn_proj_gemm_dl<MI, BK, S>, 128, 128, BK, DlCfg<2, BK, S>::kLdsBytes, NAME }
 // [0] is the default (measured fastest on MI355X: 128 x 128 tiles, k 64 per
 // stage, two LDS stages filled directly from global memory, two workgroups
-// per CU); [1] is the register-staged kernel.
-const TileShape kTiles[] = {QKN_DL(64, 2, "proj<128x128,64,dl2>"),
-                            QKN_TILE(2, 2, 64, "proj<128x128,64,reg>")};
+// per CU, 16 x 16 x 32 MFMAs); [1] is the register-staged kernel and [2] the
+// direct-to-LDS kernel on 32 x 32 x 16 MFMAs, both kept as second and third
+// implementations of the same sums (same bits).
+const TileShape kTiles[] = {QKN_DL(16, 64, 2, "proj<128x128,64,dl2,mi16>"),
+                            QKN_TILE(2, 2, 64, "proj<128x128,64,reg>"),
+                            QKN_DL(32, 64, 2, "proj<128x128,64,dl2>")};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
 // Process-wide choice of tile shape (benchmarks): 0 = automatic, i = kTiles[i - 1].

@@ -585,8 +585,8 @@ def _proj_plan(lib, T, hidden, dims):
 
 def test_proj_plan(lib):
     # whole 128 x 128 tiles at prefill sizes
-    assert _proj_plan(lib, 8192, 4096, (2048, 512)) == "proj<128x128,64,dl2>"
-    assert _proj_plan(lib, 1025, 4096, (1024,)) == "proj<128x128,64,dl2>"
+    assert _proj_plan(lib, 8192, 4096, (2048, 512)) == "proj<128x128,64,dl2,mi16>"
+    assert _proj_plan(lib, 1025, 4096, (1024,)) == "proj<128x128,64,dl2,mi16>"
     # decode sizes split k, with 64-row tiles up to 64 tokens
     assert _proj_plan(lib, 64, 4096, (1024, 256)) == "proj<64x128,64,dl4,splitk>"
     assert _proj_plan(lib, 1, 4096, (1024,)) == "proj<64x128,64,dl4,splitk>"
@@ -599,12 +599,17 @@ def test_proj_plan(lib):
         assert _proj_plan(lib, 64, 4096, (1024, 256)) == "proj<128x128,64,reg>"
     finally:
         assert lib.qkn_set_option(b"proj_tile", 0) == 0
+    assert lib.qkn_set_option(b"proj_tile", 3) == 0
+    try:
+        assert _proj_plan(lib, 8192, 4096, (2048, 512)) == "proj<128x128,64,dl2>"
+    finally:
+        assert lib.qkn_set_option(b"proj_tile", 0) == 0
 
 
 def test_proj_tile_option(lib):
-    for v in (0, 1, 2):
+    for v in (0, 1, 2, 3):
         assert lib.qkn_set_option(b"proj_tile", v) == 0
-    assert lib.qkn_set_option(b"proj_tile", 3) == L.QKN_EINVAL
+    assert lib.qkn_set_option(b"proj_tile", 4) == L.QKN_EINVAL
     assert lib.qkn_set_option(b"proj_tile", -1) == L.QKN_EINVAL
     assert lib.qkn_set_option(b"proj_tile", 0) == 0
 

@@ -174,24 +174,26 @@ def test_errors_raise():
     assert e.value.status == L.QKN_EOVERLAP
 
 
-def test_both_kernels_give_the_same_bits():
-    """The direct-to-LDS kernel and the register-staged one accumulate every
-    output in the same k order: identical y and statistics."""
+def test_all_kernels_give_the_same_bits():
+    """The direct-to-LDS kernels (16 x 16 x 32 and 32 x 32 x 16 MFMAs) and the
+    register-staged one accumulate every output over the same k-blocks in the
+    same order: identical y and statistics."""
     rng = np.random.default_rng(8)
     T, h, dq, dk = 333, 1096, 264, 136
     x = workloads.f32_to_bf16_bits(rng.standard_normal((T, h), dtype=np.float32))
     ws = [workloads.f32_to_bf16_bits(rng.standard_normal((d, h), dtype=np.float32) / 30) for d in (dq, dk)]
     outs = []
-    for choice in (1, 2):
+    for choice, suffix in ((1, "dl2,mi16>"), (2, "reg>"), (3, "dl2>")):
         L.qkn_set_option("proj_tile", choice)
         try:
             o, info = _run(x, ws)
         finally:
             L.qkn_set_option("proj_tile", 0)
-        assert info["kernel"].endswith("dl2>" if choice == 1 else "reg>"), info
+        assert info["kernel"].endswith(suffix), info
         outs.append(o)
-    for a, b in zip(*outs):
-        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
     for (y, part), w, t in zip(outs[0], ws, "qk"):
         _check(x, w, y, part, t)
 
