@@ -12,7 +12,7 @@
 //     operand. Whole tiles use v_mfma_f32_16x16x32_bf16: lane l holds row
 //     (l mod 16), k-values 8*(l/16) .. 8*(l/16)+7 of a 16 x 32 slab, and the
 //     16x16 result block leaves column (l mod 16), rows 4*(l/16) + r in
-//     accumulator r. The split-k kernels (and a selectable whole-tile one) use
+//     accumulator r. A selectable whole-tile variant uses
 //     v_mfma_f32_32x32x16_bf16: row (l mod 32), k-values 8*(l/32) .. +7 of a
 //     32 x 16 slab; result column (l mod 32), rows 8*(r/4) + 4*(l/32) +
 //     (r mod 4) in accumulator r. Both sum the same k-blocks of 16 in the same
@@ -651,6 +651,7 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_dl(const ProjParams p)
 // running the epilogue.
 template <int WMB, int BK, int S>
 __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams p) {
+  constexpr int MI = 16;  // 16 x 16 x 32 MFMAs (same bits as 32 x 32 x 16, 1-2 % faster here)
   using C = DlCfg<WMB, BK, S>;
   __shared__ __align__(1024) unsigned char lds[C::kLdsBytes];
   const int b = static_cast<int>(blockIdx.x);
@@ -661,21 +662,24 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams
   const int k_hi = (k_lo + p.kslice < p.hidden) ? k_lo + p.kslice : p.hidden;
   const TileAt t = tile_at<WMB>(p, 0, mt, nt);
   const ProjSegDev& s = p.seg[t.si];
-  f32x16 acc[WMB][2];
-  dl_mainloop<32, WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, k_lo, k_hi, acc);
-  // fp32 sums of this k-slice: lanes 0..31 of a row are 32 adjacent columns
+  using A = AccOf<MI, WMB>;
+  typename A::T acc;
+  dl_mainloop<MI, WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, k_lo, k_hi, acc);
+  // fp32 sums of this k-slice: lanes 0..MI-1 of a row are MI adjacent columns
   const int lane = static_cast<int>(threadIdx.x) & 63;
   const int wave = static_cast<int>(threadIdx.x) >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   float* part = p.part + static_cast<int64_t>(ks) * p.T * p.ncols;
 #pragma unroll
-  for (int i = 0; i < WMB; ++i)
+  for (int i = 0; i < A::kM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = wn * 64 + j * 32 + (lane & 31);
+    for (int j = 0; j < A::kN; ++j) {
+      const int col = wn * 64 + j * MI + (lane & (MI - 1));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * 32 * WMB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < A::kR; ++r) {
+        const int row = (MI == 32)
+            ? wm * 32 * WMB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)
+            : wm * 32 * WMB + i * 16 + 4 * (lane >> 4) + r;
         if (row < t.rows_a && col < t.rows_b)
           part[(t.m0 + row) * p.ncols + s.col0 + t.n0 + col] = acc[i][j][r];
       }
