@@ -780,7 +780,15 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic_bytes(info["kernel"], wl.name),
                      "algorithmic_bytes": case.bytes, "kernel_us": round(kernel_ms * 1e3, 3),
-                     "isolated_launch_us": round(isolated_ms * 1e3, 3)},
+                     "isolated_launch_us": round(isolated_ms * 1e3, 3),
+                     # a streaming copy of the same bytes in the same run: the
+                     # practical ceiling of a read-once/write-once kernel
+                     "copy_ceiling": ({"us": extras["stream_copy_same_bytes"]["us_per_step"],
+                                       "frac_of_peak": round(
+                                           extras["stream_copy_same_bytes"]["gbs"] / HBM_PEAK_GBS, 4),
+                                       "kernel_frac_of_copy":
+                                           extras["stream_copy_same_bytes"]["fused_kernel_frac_of_copy"]}
+                                      if "stream_copy_same_bytes" in extras else None)},
         "cpu_baseline": cpu,
         "extras": extras,
     }
