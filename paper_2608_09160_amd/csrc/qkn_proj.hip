@@ -15,8 +15,9 @@
 //     accumulator r. A selectable whole-tile variant uses
 //     v_mfma_f32_32x32x16_bf16: row (l mod 32), k-values 8*(l/32) .. +7 of a
 //     32 x 16 slab; result column (l mod 32), rows 8*(r/4) + 4*(l/32) +
-//     (r mod 4) in accumulator r. Both sum the same k-blocks of 16 in the same
-//     order per output (measured: bit-identical results).
+//     (r mod 4) in accumulator r. Both walk k in ascending order per output,
+//     and the two instructions round their exact bf16 products identically:
+//     the results are bit-identical (checked on every tested shape).
 //   * A 256-thread workgroup owns a 128 x 128 output tile (four wavefronts in
 //     2 x 2, 64 x 64 each = 4 x 4 or 2 x 2 MFMA blocks); k advances 64 at a time
 //     through two LDS stages that global memory fills directly (buffer_load
