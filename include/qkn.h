@@ -185,7 +185,12 @@ int qkn_full_fp8(const qkn_seg8* segs, int nseg, int64_t T, float eps, void* str
  * round's epoch in the high half, written by one aligned 64-bit store, so a
  * reader that sees the epoch also sees the value. Slot arrays are uint64
  * [tp * T], rank-major (slot k*T + t), one per tensor; they need no reset
- * between rounds: each round uses a new nonzero epoch.
+ * between rounds: each round uses a new nonzero epoch. The epoch is an
+ * argument of the launch, so a HIP graph that captured a waiting launch keeps
+ * its epoch: replaying it would accept the slots that an earlier replay
+ * published. Such a graph needs its slot arrays cleared to zero (epoch 0 is
+ * never a round's) at the start of every replay, e.g. by a fill kernel
+ * captured before the producers' launches, or one graph per round.
  */
 
 /*
