@@ -4,10 +4,10 @@ replays are separated by eager work that overwrites the outputs, so a replay
 that wrote nothing, or wrote stale values, is caught. The library allocates
 nothing and records no memset, so its launches are capturable as they are.
 
-Not covered here: the Phase B wait entry points, whose round epoch is an
-argument of the launch; a captured launch keeps its epoch, so a graph of
-waiting launches can only be replayed if the slots are re-armed between
-replays (see qkn.h).
+The Phase B wait entry points take the round's epoch as a launch argument,
+which a captured launch keeps; their graph clears the slot arrays with a
+fill kernel before the waiting launch (the recipe qkn.h gives), and the
+test plants stale slots carrying that epoch between replays.
 """
 from __future__ import annotations
 
@@ -101,3 +101,38 @@ def test_projection_graph_replays(T, hidden, dq, dk):
             s.partials.fill_(float(r))
         prep.workspace.fill_(0xFF)
     _check_replays(prep, outs, clobber)
+
+
+@pytest.mark.parametrize("wl", [workloads.DECODE_TP4, workloads.DECODE_TP8.with_dtype("fp8")],
+                         ids=lambda w: w.name)
+def test_group_wait_graph_with_slots_cleared_in_the_graph(wl):
+    """A whole tp group in one waiting launch, captured after a fill kernel
+    that clears the slot arrays. Between replays the slots are overwritten
+    eagerly with wrong statistics that carry the captured epoch: a replay that
+    did not clear them first would accept those. Every replay equals eager."""
+    print(f"[graph] group wait {wl.name}", flush=True)
+    data = inputs(wl)
+    slots = [torch.zeros((wl.tp, wl.T), dtype=torch.int64, device=DEV) for _ in range(2)]
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    segs = []
+    for key, gkey, d_full in (("xq", "gq", wl.q_full), ("xk", "gk", wl.k_full)):
+        x = to_dev_act(data[key])
+        segs.append(L.Seg(x=x, w=to_dev_f32(data[gkey]), d_full=d_full, y=torch.empty_like(x),
+                          inv_rms=torch.empty((wl.tp, wl.T), dtype=torch.float32, device=DEV)))
+    epoch = 21
+
+    def step():
+        for s in slots:
+            s.zero_()  # a fill kernel (no memset node): epoch 0 is never a round's
+        L.qkn_fused_group_wait(segs, wl.tp, wl.eps, slots, epoch=epoch, spin_limit=1 << 20,
+                               status=status)
+    stale = (epoch << 32) | 0x3F800000  # statistic 1.0 with the captured epoch
+
+    def clobber(r):
+        for s in segs:
+            s.y.view(torch.uint8).fill_(0x7F)
+            s.inv_rms.fill_(float(r))
+        for s in slots:
+            s.fill_(stale)
+    _check_replays(step, [s.y for s in segs] + [s.inv_rms for s in segs], clobber)
+    assert int(status.item()) == 0
