@@ -113,8 +113,15 @@ def _check(status: int, where: str) -> None:
         raise QknError(status, where)
 
 
+# torch's raw current-stream query (no Stream object is built: a third of
+# the host time of a prepared launch otherwise); the public call if absent
+_raw_current_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
+        if _raw_current_stream is not None:
+            return _raw_current_stream(torch.cuda.current_device())
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
