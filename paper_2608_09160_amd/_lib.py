@@ -388,6 +388,35 @@ class Prepared:
         _check(rc, self.name)
 
 
+class PreparedApply:
+    """qkn_apply (or qkn_apply_fp8, by the activations' dtype) with its
+    arguments checked and marshalled once, for repeated launches on the same
+    tensors (the Phases B+C after qkn_proj_partial in a serving loop). The
+    tensors stay referenced for the object's lifetime."""
+
+    def __init__(self, x: torch.Tensor, w: torch.Tensor, partials: torch.Tensor, d_full: int,
+                 eps: float, y: Optional[torch.Tensor] = None,
+                 inv_rms: Optional[torch.Tensor] = None):
+        fmt = _fmt_of(x)
+        self.name = "qkn_apply" + ("_fp8" if fmt == FP8 else "")
+        px, ldx, T, d = _rows(x, "x", fmt)
+        if partials.dim() != 2 or partials.shape[1] != T:
+            raise ValueError(f"partials: expected [tp, {T}], got {tuple(partials.shape)}")
+        if y is None:
+            y = torch.empty((T, d), dtype=x.dtype, device=x.device)
+        py, ldy, Ty, dy = _rows(y, "y", fmt)
+        if (Ty, dy) != (T, d):
+            raise ValueError("y: shape must match x")
+        self.x, self.w, self.partials, self.y, self.inv_rms = x, w, partials, y, inv_rms
+        self._args = (px, ldx, _f32(w, "w", d), _f32(partials, "partials"), partials.shape[0], T,
+                      d, d_full, eps, py, ldy, _f32(inv_rms, "inv_rms", T))
+        self._fn = getattr(load(), self.name)
+
+    def __call__(self, stream=None) -> torch.Tensor:
+        _check(self._fn(*self._args, _stream(stream)), self.name)
+        return self.y
+
+
 @dataclass
 class ProjSeg:
     """One projection output (Q or K) of one rank for qkn_proj_partial."""

@@ -136,3 +136,31 @@ def test_group_wait_graph_with_slots_cleared_in_the_graph(wl):
             s.fill_(stale)
     _check_replays(step, [s.y for s in segs] + [s.inv_rms for s in segs], clobber)
     assert int(status.item()) == 0
+
+
+@pytest.mark.parametrize("wl,rank", [(workloads.DECODE_TP4, 3), (workloads.DECODE_TP4.with_dtype("fp8"), 0)],
+                         ids=lambda v: getattr(v, "name", str(v)))
+def test_prepared_apply_equals_apply_and_replays(wl, rank):
+    """PreparedApply (arguments marshalled once) gives qkn_apply's bits, eager
+    and from a replayed graph."""
+    print(f"[graph] prepared apply {wl.name} rank {rank}", flush=True)
+    data = inputs(wl)
+    cols = workloads.shard_cols(wl.q_full, wl.tp, rank)
+    x = to_dev_act(data["xq"][:, cols])
+    w = to_dev_f32(data["gq"][cols])
+    P = peer_partials(data, "xq", wl.q_full, wl.tp, wl.T, rank)
+    (L.qkn_partial_sumsq_fp8 if wl.dtype == "fp8" else L.qkn_partial_sumsq)(x, out=P[rank])
+    inv = torch.empty(wl.T, dtype=torch.float32, device=DEV)
+    ref_y = (L.qkn_apply_fp8 if wl.dtype == "fp8" else L.qkn_apply)(x, w, P, wl.q_full, wl.eps,
+                                                                     inv_rms=inv)
+    ref = _outputs([ref_y, inv])
+    prep = L.PreparedApply(x, w, P, wl.q_full, wl.eps,
+                           inv_rms=torch.empty(wl.T, dtype=torch.float32, device=DEV))
+    got = _outputs([prep(), prep.inv_rms])
+    for a, b in zip(ref, got):
+        assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+
+    def clobber(r):
+        prep.y.view(torch.uint8).fill_(0x7F)
+        prep.inv_rms.fill_(float(r))
+    _check_replays(prep, [prep.y, prep.inv_rms], clobber)
