@@ -410,15 +410,6 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm(const ProjParams p) {
   epilogue<WMB, WNB, C::kOutRow>(p, s, acc, lds, m0, n0, rows_a, rows_b);
 }
 
-// Direct-to-LDS variant: each stage's operand tiles go from global memory
-// straight into LDS (buffer_load ... lds: lane l's 16 bytes land at the
-// instruction's LDS base + 16 l), through a ring of S stages, so the loads of
-// stage kt + S - 1 are in flight while stage kt is computed and no VGPRs stage
-// the data. Rows are not padded; instead the 16-byte k-slot of each row is
-// XOR-swizzled, slot' = slot ^ ((row / (16 / P)) mod P) with P = BK / 8 slots
-// per row, which puts the 16 rows read by a 16-lane group at 16 distinct
-// 16-byte bank groups. Lane l of a load instruction therefore fetches the
-// global k-vector that belongs at its fixed LDS slot.
 // Accumulators of a wavefront's (32 WMB) x 64 share of a tile: MI x MI MFMA
 // blocks, kM x kN of them, kR fp32 values per lane each.
 template <int MI, int WMB>
@@ -434,6 +425,15 @@ struct AccOf<16, WMB> {
   typedef f32x4 T[kM][kN];
 };
 
+// Direct-to-LDS variant: each stage's operand tiles go from global memory
+// straight into LDS (buffer_load ... lds: lane l's 16 bytes land at the
+// instruction's LDS base + 16 l), through a ring of S stages, so the loads of
+// stage kt + S - 1 are in flight while stage kt is computed and no VGPRs stage
+// the data. Rows are not padded; instead the 16-byte k-slot of each row is
+// XOR-swizzled, slot' = slot ^ ((row / (16 / P)) mod P) with P = BK / 8 slots
+// per row, which puts the 16 rows read by a 16-lane group at 16 distinct
+// 16-byte bank groups. Lane l of a load instruction therefore fetches the
+// global k-vector that belongs at its fixed LDS slot.
 template <int WMB, int BK, int S>
 struct DlCfg {
   static constexpr int BM = 64 * WMB, BN = 128;        // tile rows (tokens), columns
@@ -481,9 +481,9 @@ __device__ __forceinline__ void vm_wait(int n) {
 // Main loop of one direct-to-LDS tile: BM = 64 WMB rows from m0 (rows_a of
 // them valid) by 128 columns from n0 of segment s (rows_b valid), k in
 // [k_lo, k_hi). Four wavefronts in a 2 x 2 grid, each (32 WMB) x 64, i.e.
-// WMB x 2 MFMA blocks of 32 x 32; every accumulator takes its k-blocks of 16
-// in ascending order whatever the tile's height, so all tile shapes give the
-// same bits.
+// WMB x 2 MFMA blocks of 32 x 32 (MI = 32) or 2 WMB x 4 blocks of 16 x 16
+// (MI = 16); every accumulator takes k in ascending order whatever the
+// tile's height, so all tile shapes give the same bits.
 template <int MI, int WMB, int BK, int S>
 __device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDev& s,
                                             unsigned char* lds, int64_t m0, int n0, int rows_a,
