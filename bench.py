@@ -329,15 +329,16 @@ def trace_name(launch_name: str) -> str:
     """Profiler (demangled) name of the kernel a launch name denotes, e.g.
     "rows<4,1>/fused" -> "void qkn_rows<FmtBf16, 4, 1, 0, 0>"."""
     import re
-    m = re.fullmatch(r"(rows|rows_pf|rows_pa|rows_pa2|rows_pa3|rows_fp8|wide|wide_fp8)<(\d+),(\d+)>/(\w+)", launch_name)
-    if not m:
+    m = re.fullmatch(r"(rows|wide)(_pf|_pa|_pa2|_pa3)?(_fp8)?<(\d+),(\d+)>/"
+                     r"(fused|apply|partial|fused_wait|publish)", launch_name)
+    if not m or (m.group(1) == "wide" and m.group(2)):
         raise ValueError(f"no profiler name for {launch_name!r}")
-    fam, n0, n1, mode = m.groups()
-    fmt = "FmtFp8" if fam.endswith("fp8") else "FmtBf16"
+    fam, sched_tag, fp8, n0, n1, mode = m.groups()
+    fmt = "FmtFp8" if fp8 else "FmtBf16"
     mode_id = ["fused", "apply", "partial", "fused_wait", "publish"].index(mode)
-    if fam.startswith("wide"):
+    if fam == "wide":
         return f"void qkn_wide<{fmt}, {n0}, {n1}, {mode_id}>"
-    sched = {"rows_pf": 1, "rows_pa": 2, "rows_pa2": 3, "rows_pa3": 4}.get(fam, 0)
+    sched = {None: 0, "_pf": 1, "_pa": 2, "_pa2": 3, "_pa3": 4}[sched_tag]
     return f"void qkn_rows<{fmt}, {n0}, {n1}, {mode_id}, {sched}>"
 
 
