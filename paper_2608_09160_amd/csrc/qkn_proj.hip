@@ -757,13 +757,27 @@ __global__ __launch_bounds__(64 * kReduceWaves) void qkn_proj_reduce(const ProjP
 }
 
 // partials[t] = chunk statistics of token t added in ascending chunk order.
+// The loads go out sixteen at a time before their sums (a plain loop waited
+// for each load before the next add: 6.0 us for the prefill shard, 4.6 us
+// batched).
 __global__ __launch_bounds__(256) void qkn_proj_finish(const ProjParams p) {
+  constexpr int kBatch = 16;
   const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int si = static_cast<int>(blockIdx.y);
   if (t >= p.T || si >= p.nseg) return;
   const ProjSegDev& s = p.seg[si];
-  float S = s.tile_partials[t];
-  for (int n = 1; n < s.nchunks; ++n) S = S + s.tile_partials[static_cast<int64_t>(n) * p.T + t];
+  const float* src = s.tile_partials + t;
+  const int nc = s.nchunks;
+  float S = 0.0f;
+  for (int n = 0; n < nc; n += kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      v[j] = (n + j < nc) ? src[static_cast<int64_t>(n + j) * p.T] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      if (n + j < nc) S = (n + j == 0) ? v[j] : S + v[j];  // chunk 0 starts the sum
+  }
   s.partials[t] = S;
 }
 
