@@ -388,6 +388,26 @@ class Prepared:
         _check(rc, self.name)
 
 
+class PreparedPartial:
+    """qkn_partial_sumsq (or _fp8, by the activations' dtype) with its arguments
+    checked and marshalled once, for repeated launches on the same tensors.
+    The tensors stay referenced for the object's lifetime."""
+
+    def __init__(self, x: torch.Tensor, out: Optional[torch.Tensor] = None):
+        fmt = _fmt_of(x)
+        self.name = "qkn_partial_sumsq" + ("_fp8" if fmt == FP8 else "")
+        px, ldx, T, d = _rows(x, "x", fmt)
+        if out is None:
+            out = torch.empty(T, dtype=torch.float32, device=x.device)
+        self.x, self.out = x, out
+        self._args = (px, ldx, T, d, _f32(out, "out", T))
+        self._fn = getattr(load(), self.name)
+
+    def __call__(self, stream=None) -> torch.Tensor:
+        _check(self._fn(*self._args, _stream(stream)), self.name)
+        return self.out
+
+
 class PreparedApply:
     """qkn_apply (or qkn_apply_fp8, by the activations' dtype) with its
     arguments checked and marshalled once, for repeated launches on the same

@@ -141,8 +141,8 @@ def test_group_wait_graph_with_slots_cleared_in_the_graph(wl):
 @pytest.mark.parametrize("wl,rank", [(workloads.DECODE_TP4, 3), (workloads.DECODE_TP4.with_dtype("fp8"), 0)],
                          ids=lambda v: getattr(v, "name", str(v)))
 def test_prepared_apply_equals_apply_and_replays(wl, rank):
-    """PreparedApply (arguments marshalled once) gives qkn_apply's bits, eager
-    and from a replayed graph."""
+    """PreparedPartial and PreparedApply (arguments marshalled once) give
+    qkn_partial_sumsq's and qkn_apply's bits, eager and from a replayed graph."""
     print(f"[graph] prepared apply {wl.name} rank {rank}", flush=True)
     data = inputs(wl)
     cols = workloads.shard_cols(wl.q_full, wl.tp, rank)
@@ -154,6 +154,8 @@ def test_prepared_apply_equals_apply_and_replays(wl, rank):
     ref_y = (L.qkn_apply_fp8 if wl.dtype == "fp8" else L.qkn_apply)(x, w, P, wl.q_full, wl.eps,
                                                                      inv_rms=inv)
     ref = _outputs([ref_y, inv])
+    part = L.PreparedPartial(x)
+    assert torch.equal(part(), P[rank])  # the prepared Phase A gives the same statistic
     prep = L.PreparedApply(x, w, P, wl.q_full, wl.eps,
                            inv_rms=torch.empty(wl.T, dtype=torch.float32, device=DEV))
     got = _outputs([prep(), prep.inv_rms])
