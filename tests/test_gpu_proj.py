@@ -56,7 +56,8 @@ def _check(x_bits, w_bits, y_bits, part, what):
 
 @pytest.mark.parametrize("T,hidden,dq,dk", [(300, 4096, 2048, 512), (1, 64, 8, 0), (129, 136, 200, 72),
                                              (77, 1000, 128, 8), (256, 2048, 1024, 256),
-                                             (5, 8, 16, 0), (130, 4104, 136, 0)])
+                                             (5, 8, 16, 0), (130, 4104, 136, 0), (37, 520, 264, 40),
+                                             (64, 8192, 8, 2040)])
 def test_projection_matches_oracle(T, hidden, dq, dk):
     rng = np.random.default_rng(T * 31 + hidden)
     x = workloads.f32_to_bf16_bits(rng.standard_normal((T, hidden), dtype=np.float32))
