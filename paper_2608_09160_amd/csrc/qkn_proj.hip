@@ -45,7 +45,7 @@
 //     CUs idle) split k: separate workgroups take contiguous k-slices of each
 //     tile (64-row tiles up to 64 tokens; four LDS stages, so a slice's loads
 //     are all in flight at once) and store their fp32 sums; one reduction
-//     launch, a workgroup per token, adds the slices in ascending order,
+//     launch, a workgroup per token and segment, adds the slices in ascending order,
 //     rounds once, writes y and takes the statistic with the same tree.
 
 #include <hip/hip_runtime.h>
@@ -687,8 +687,10 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams
     }
 }
 
-// Split-k reduction, one workgroup per token, one wavefront per 128-column
-// chunk (wavefront w takes chunks w, w + waves, ...): each lane adds two
+// Split-k reduction, one workgroup per token and segment (the segments'
+// statistics are separate sums, so Q and K run on different CUs), one
+// wavefront per 128-column chunk (wavefront w takes chunks w, w + waves,
+// ...): each lane adds two
 // columns' k-slice sums in ascending slice order and rounds them once to bf16
 // (y); the chunk's statistic follows the tile epilogue's tree (two ascending
 // FMA chains over the chunk's halves, first + second); after a barrier the
@@ -701,16 +703,14 @@ __global__ __launch_bounds__(64 * kReduceWaves) void qkn_proj_reduce(const ProjP
   __shared__ float vals[kReduceWaves][kChunkN];
   __shared__ float chunk_sum[kMaxSplitChunks];
   const int64_t t = blockIdx.x;
+  const int si = static_cast<int>(blockIdx.y);
+  const ProjSegDev& s = p.seg[si];
   const int tid = static_cast<int>(threadIdx.x);
   const int lane = tid & 63, wave = tid >> 6;
   const int waves = static_cast<int>(blockDim.x) >> 6;
-  const int total = p.seg[0].nchunks + (p.nseg == 2 ? p.seg[1].nchunks : 0);
   const int64_t slice = p.T * p.ncols;
   float* v = vals[wave];
-  for (int g = wave; g < total; g += waves) {
-    const int si = (g >= p.seg[0].nchunks) ? 1 : 0;
-    const ProjSegDev& s = p.seg[si];
-    const int q = g - (si ? p.seg[0].nchunks : 0);
+  for (int q = wave; q < s.nchunks; q += waves) {
     const int c = q * kChunkN + 2 * lane;  // d_local is a multiple of 8: c < d means c + 1 < d
     float v0 = 0.0f, v1 = 0.0f;
     if (c < s.d) {
@@ -742,16 +742,14 @@ __global__ __launch_bounds__(64 * kReduceWaves) void qkn_proj_reduce(const ProjP
     for (int i = 0; i < 64; ++i) acc_s = __builtin_fmaf(h[i], h[i], acc_s);
     const float other = __builtin_bit_cast(
         float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc_s), 0xB1, 0xF, 0xF, false));
-    if (lane == 0) chunk_sum[g] = acc_s + other;
+    if (lane == 0) chunk_sum[q] = acc_s + other;
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();  // the row is read before the next chunk overwrites it
   }
   __syncthreads();
-  if (tid < p.nseg) {
-    const ProjSegDev& s = p.seg[tid];
-    const float* cs = chunk_sum + (tid ? p.seg[0].nchunks : 0);
-    float S = cs[0];
-    for (int n = 1; n < s.nchunks; ++n) S = S + cs[n];
+  if (tid == 0) {
+    float S = chunk_sum[0];
+    for (int n = 1; n < s.nchunks; ++n) S = S + chunk_sum[n];
     s.partials[t] = S;
   }
 }
@@ -1006,13 +1004,15 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
       hipSuccess)
     return QKN_EHIP;
   if (split) {
-    const int waves = pl.chunks < kReduceWaves ? static_cast<int>(pl.chunks) : kReduceWaves;
+    int64_t most = 0;  // chunks of the widest segment: one wavefront each, up to kReduceWaves
+    for (int i = 0; i < nseg; ++i) most = p.seg[i].nchunks > most ? p.seg[i].nchunks : most;
+    const int waves = most < kReduceWaves ? static_cast<int>(most) : kReduceWaves;
     const void* reduce = pl.splits == 2   ? reinterpret_cast<const void*>(qkn_proj_reduce<2>)
                          : pl.splits == 4 ? reinterpret_cast<const void*>(qkn_proj_reduce<4>)
                          : pl.splits == 8 ? reinterpret_cast<const void*>(qkn_proj_reduce<8>)
                                           : reinterpret_cast<const void*>(qkn_proj_reduce<16>);
-    if (hipLaunchKernel(reduce,
-                        dim3(static_cast<unsigned>(T)), dim3(64 * waves), args, 0, st) != hipSuccess)
+    if (hipLaunchKernel(reduce, dim3(static_cast<unsigned>(T), static_cast<unsigned>(nseg)),
+                        dim3(64 * waves), args, 0, st) != hipSuccess)
       return QKN_EHIP;
   } else {
     const dim3 fgrid(static_cast<unsigned>((T + 255) / 256), static_cast<unsigned>(nseg));
