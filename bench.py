@@ -461,7 +461,11 @@ def summarize(outdir: str) -> None:
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 
 
-def proj_extra(torch, L, workloads, wl, rank, steps=50):
+def proj_extra(torch, L, workloads, wl, rank, steps=50, graph=False):
+    """The Q/K projection with the statistic against torch.mm. graph=True times
+    replays of a captured graph (decode sizes, where back-to-back eager calls
+    are bound by the host) and prices the launch against the HBM roofline
+    (streaming W dominates); otherwise eager launches against the MFMA peak."""
     dev = "cuda:0"
 
     def bf16(a):
@@ -475,20 +479,31 @@ def proj_extra(torch, L, workloads, wl, rank, steps=50):
     flops = 2 * wl.T * hidden * (wq.shape[0] + wk.shape[0])
     prep = L.PreparedProj(x, [L.ProjSeg(w=wq), L.ProjSeg(w=wk)])
     wqk_t = torch.cat([wq, wk]).t().contiguous()
+    def timed(fn):  # ms per call
+        if graph:
+            return time_graph(torch, fn, steps, 10)
+        return time_region(torch, fn, steps, 10) / steps
     ours, lib = [], []
     for _ in range(5):  # alternate, median of five regions each
-        ours.append(time_region(torch, lambda i: prep(), steps, 10) / steps)
-        lib.append(time_region(torch, lambda i: torch.mm(x, wqk_t), steps, 10) / steps)
+        ours.append(timed(lambda i: prep()))
+        lib.append(timed(lambda i: torch.mm(x, wqk_t)))
     prep()
     info = L.qkn_last_launch()
     t, tm = float(np.median(ours)), float(np.median(lib))
     tf = flops / (t * 1e-3) / 1e12
+    cols = wq.shape[0] + wk.shape[0]
+    if graph:
+        nbytes = 2 * (cols * hidden + wl.T * hidden + wl.T * cols)  # W, x, y in bf16
+        gbs = nbytes / (t * 1e-3) / 1e9
+        roof = {"bound": "hbm", "bytes": nbytes, "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    else:
+        roof = {"bound": "mfma", "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
     return {"kernel": info["kernel"], "grid": info["grid"], "tokens": wl.T, "hidden": hidden,
-            "columns": wq.shape[0] + wk.shape[0], "flops": flops, "kernel_us": round(t * 1e3, 2),
-            "tflops": round(tf, 1), "roofline": {"bound": "mfma", "peak": MFMA_BF16_PEAK_TFLOPS,
-                                                  "unit": "TFLOP/s",
-                                                  "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)},
-            "torch_mm_us": round(tm * 1e3, 2),
+            "columns": cols, "flops": flops, "kernel_us": round(t * 1e3, 2),
+            "timing": "graph replay" if graph else "eager", "tflops": round(tf, 1),
+            "roofline": roof, "torch_mm_us": round(tm * 1e3, 2),
             "torch_mm_tflops": round(flops / (tm * 1e-3) / 1e12, 1)}
 
 
@@ -757,6 +772,9 @@ def main():
         # cores, with the statistic taken from each output tile; against
         # torch.mm (hipBLASLt) of the same product without the statistic
         extras["proj_partial_prefill"] = proj_extra(torch, L, workloads, wl, args.rank)
+        # the same at decode size: 64 tokens, Q 1024 + K 256 columns (tp 4)
+        extras["proj_partial_decode"] = proj_extra(torch, L, workloads, workloads.DECODE_TP4, 1,
+                                                   steps=20, graph=True)
         print("[bench] extras done", file=sys.stderr, flush=True)
 
     cpu = None
