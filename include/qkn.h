@@ -63,6 +63,8 @@ extern "C" {
 #define QKN_EOVERLAP (-2) /* an output overlaps an input or another output in part */
 #define QKN_EHIP (-3)     /* the HIP runtime refused a query or a launch */
 #define QKN_ENOTSUP (-4)  /* shape/alignment outside what this entry point supports */
+#define QKN_EDRYRUN (-5)  /* "validate_only" is set on the calling thread: the arguments
+                             were accepted and a kernel chosen, but nothing was launched */
 
 /*
  * One tensor (Q or K) of one rank.
@@ -205,10 +207,18 @@ int qkn_full_fp8(const qkn_seg8* segs, int nseg, int64_t T, float eps, void* str
 int qkn_publish_partials(const uint16_t* x, int64_t ldx, int64_t T, int64_t d_local,
                          uint64_t* slots_out, uint32_t epoch, void* stream);
 
+/*
+ * Largest spin_limit: about 4 million polls of one slot, each a round trip to
+ * memory after a short sleep, i.e. seconds at most before a wavefront whose
+ * peer never publishes gives up -- so a wait stays bounded whatever the
+ * caller asks for.
+ */
+#define QKN_MAX_SPIN_LIMIT (INT64_C(1) << 22)
+
 typedef struct qkn_wait {
   uint64_t* slots[2];  /* per segment: slot array [tp * T] (see above) */
   uint32_t epoch;      /* nonzero: the slots of this round carry it */
-  int64_t spin_limit;  /* polls of one slot before giving up (>= 1) */
+  int64_t spin_limit;  /* polls of one slot before giving up, 1..QKN_MAX_SPIN_LIMIT */
   int co_resident;     /* kernels on this GPU that wait on each other (>= 1): the
                           grid is sized so that all of their wavefronts are
                           resident together (Sec. III-D's bound) */
@@ -225,9 +235,12 @@ typedef struct qkn_wait {
  * statistics. A wait that exceeds spin_limit polls sets *status = 1 and the
  * wavefront stops waiting for its later tokens; every kernel exits normally.
  * segs[i].partials must be NULL (statistics travel in the slots).
- * QKN_EINVAL: as qkn_fused_shard, and wait NULL, epoch 0, spin_limit < 1,
- * co_resident < 1, a NULL or misaligned slot array or status, partials set.
- * QKN_ENOTSUP: a segment outside the register path (see qkn_publish_partials).
+ * QKN_EINVAL: as qkn_fused_shard, and wait NULL, epoch 0, spin_limit < 1 or
+ * > QKN_MAX_SPIN_LIMIT, co_resident < 1, a NULL or misaligned slot array or
+ * status, partials set.
+ * QKN_ENOTSUP: a segment outside the register path (see qkn_publish_partials),
+ * or tp * T * 8 >= 2^31 (the kernel addresses a token's slots by 32-bit byte
+ * offsets from rank 0's).
  * QKN_EOVERLAP: slot arrays or status overlapping anything else.
  */
 int qkn_fused_shard_wait(const qkn_seg* segs, int nseg, int tp, int rank, int64_t T, float eps,
@@ -269,7 +282,8 @@ int qkn_fused_group_wait_fp8(const qkn_seg8* segs, int nseg, int tp, int64_t T, 
 const char* qkn_strerror(int status);
 
 /*
- * Launch description of the calling thread's most recent successful launch,
+ * Launch description of the calling thread's most recent successful launch (or
+ * validate_only call, with grid 0),
  * for tests and benchmarks. kernel is a static string naming the variant
  * ("rows<4,1>/fused", "wide<16,2>/fused", "generic/apply", "rows_fp8<2,1>/fused",
  * ...; the numbers are 16-byte chunks per lane); grid is in workgroups, block in
@@ -286,8 +300,10 @@ typedef struct qkn_launch_info {
 int qkn_last_launch(qkn_launch_info* info);
 
 /*
- * Process-wide tuning knobs (for benchmarks and tests; not thread-safe with
- * concurrent launches). Keys:
+ * Tuning knobs for benchmarks and tests. Each setting applies only to launches
+ * made later from the calling thread (options are thread-local: a setting in
+ * one thread never changes another thread's launches); a new thread starts
+ * with the defaults. Keys:
  *   "waves_per_cu"   wavefronts per CU used to size the grid (0 = the
  *                    default: enough to keep ~24 KB (bf16) or ~28 KB (fp8)
  *                    of rows requested per CU, at least 6, at most the
@@ -319,7 +335,10 @@ int qkn_last_launch(qkn_launch_info* info);
  *                    give the same results as 1);
  *   "validate_only"  1 = entry points validate their arguments and choose a
  *                    kernel (reported by qkn_last_launch, grid 0) but make no
- *                    HIP call and launch nothing.
+ *                    HIP call, launch nothing and return QKN_EDRYRUN (never
+ *                    QKN_OK, so a caller that checks the status cannot take
+ *                    a call that launched nothing for one that ran; calls
+ *                    with T == 0 still return QKN_OK).
  * Returns QKN_OK or QKN_EINVAL for an unknown key or a bad value.
  */
 int qkn_set_option(const char* key, int64_t value);

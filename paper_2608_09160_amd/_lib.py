@@ -23,7 +23,7 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqkn.so")
 
-QKN_OK, QKN_EINVAL, QKN_EOVERLAP, QKN_EHIP, QKN_ENOTSUP = 0, -1, -2, -3, -4
+QKN_OK, QKN_EINVAL, QKN_EOVERLAP, QKN_EHIP, QKN_ENOTSUP, QKN_EDRYRUN = 0, -1, -2, -3, -4, -5
 
 _c_i64 = ctypes.c_int64
 _vp = ctypes.c_void_p

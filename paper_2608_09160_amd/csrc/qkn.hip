@@ -95,15 +95,16 @@ const char* wide_name(int fmt, int mode, int i0, int i1) {
   return names[fmt][mode][i0][i1];
 }
 
-// Options.
-int64_t g_opt_waves_per_cu = 0;
-int64_t g_opt_wait_schedule = 4;  // publish three tokens ahead
-int64_t g_opt_waves_per_block = 0;
-int64_t g_opt_force_generic = 0;
-int64_t g_opt_validate_only = 0;
-int64_t g_opt_prefetch = 0;
-int64_t g_opt_token_blocks = 0;
-int64_t g_opt_balance = 0;
+// Options (qkn_set_option): per calling thread, so that a setting made by
+// one thread (a test, a tuning sweep) never changes another thread's launches.
+thread_local int64_t g_opt_waves_per_cu = 0;
+thread_local int64_t g_opt_wait_schedule = 4;  // publish three tokens ahead
+thread_local int64_t g_opt_waves_per_block = 0;
+thread_local int64_t g_opt_force_generic = 0;
+thread_local int64_t g_opt_validate_only = 0;
+thread_local int64_t g_opt_prefetch = 0;
+thread_local int64_t g_opt_token_blocks = 0;
+thread_local int64_t g_opt_balance = 0;
 
 thread_local qkn_launch_info t_last = {nullptr, 0, 0, 0, 0};
 
@@ -300,8 +301,12 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
     kp.group = wa->group;
   }
   const int group = (waits && wa->group > 1) ? wa->group : 1;
+  // the register path addresses a token's statistic slots by 32-bit byte
+  // offsets from rank 0's: 4-byte statistics, or 8-byte flagged slots
+  const int slot_bytes = waits ? 8 : 4;
   const bool buffer_ok = (g_opt_force_generic == 0) && tp <= kMaxFastTp &&
-                         static_cast<__int128>(tp) * T * 4 < (static_cast<__int128>(1) << 31);
+                         static_cast<__int128>(tp) * T * slot_bytes <
+                             (static_cast<__int128>(1) << 31);
   bool fast = buffer_ok;
   bool wide = buffer_ok && !waits;
   int idx[2] = {0, 0};
@@ -382,7 +387,7 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
   if (!fn) return QKN_ENOTSUP;  // not reached: every selectable entry is instantiated
   if (g_opt_validate_only) {  // arguments accepted and a kernel chosen; no HIP call
     t_last = qkn_launch_info{name, 0, 0, 0, lds};
-    return QKN_OK;
+    return QKN_EDRYRUN;
   }
 
   int dev = 0, cus = 0;
@@ -567,7 +572,9 @@ int wait_impl(const S* segs_in, int nseg, int tp, int rank, int64_t T, float eps
   if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
   int rc = validate_common(T, eps, tp, rank);
   if (rc != QKN_OK) return rc;
-  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->spin_limit > QKN_MAX_SPIN_LIMIT ||
+      wait->co_resident < 1)
+    return QKN_EINVAL;
   HSeg segs[2];
   for (int i = 0; i < nseg; ++i) {
     segs[i] = to_hseg(segs_in[i]);
@@ -605,7 +612,9 @@ int group_impl(const S* segs_in, int nseg, int tp, int64_t T, float eps, const q
   if (!segs_in || nseg < 1 || nseg > 2 || !wait) return QKN_EINVAL;
   int rc = validate_common(T, eps, tp, 0);
   if (rc != QKN_OK) return rc;
-  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->co_resident < 1) return QKN_EINVAL;
+  if (wait->epoch == 0 || wait->spin_limit < 1 || wait->spin_limit > QKN_MAX_SPIN_LIMIT ||
+      wait->co_resident < 1)
+    return QKN_EINVAL;
   HSeg segs[2];
   HSeg view[2];  // the full tensors, for shape and overlap checks
   for (int i = 0; i < nseg; ++i) {
@@ -734,6 +743,7 @@ const char* qkn_strerror(int status) {
     case QKN_EOVERLAP: return "output overlaps an input or another output";
     case QKN_EHIP: return "HIP runtime error";
     case QKN_ENOTSUP: return "shape or alignment not supported by this entry point";
+    case QKN_EDRYRUN: return "validated only: validate_only is set on this thread, nothing launched";
     default: return "unknown status";
   }
 }

@@ -41,7 +41,7 @@ int qkn_calib_copy(const void* x, void* y, int64_t bytes, int64_t blocks, void* 
   const qkn_launch_info info{"calib_copy", blocks, 256, blocks * 4, 0};
   if (qkn_host::validate_only()) {
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, 0});
-    return QKN_OK;
+    return QKN_EDRYRUN;
   }
   hipLaunchKernelGGL(qkn_calib_copy_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(x),
@@ -55,7 +55,7 @@ int qkn_calib_empty(void* stream) {
   const qkn_launch_info info{"calib_empty", 1, 64, 1, 0};
   if (qkn_host::validate_only()) {
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, 0});
-    return QKN_OK;
+    return QKN_EDRYRUN;
   }
   hipLaunchKernelGGL(qkn_calib_empty_kernel, dim3(1), dim3(64), 0,
                      static_cast<hipStream_t>(stream));

@@ -809,8 +809,9 @@ const TileShape kTiles[] = {QKN_DL(16, 64, 2, "proj<128x128,64,dl2,mi16>"),
                             QKN_DL(32, 64, 2, "proj<128x128,64,dl2>")};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
-// Process-wide choice of tile shape (benchmarks): 0 = automatic, i = kTiles[i - 1].
-int g_tile_choice = 0;
+// Choice of tile shape (benchmarks), per calling thread as every option:
+// 0 = automatic, i = kTiles[i - 1].
+thread_local int g_tile_choice = 0;
 
 const TileShape& choose_tile() {
   if (g_tile_choice > 0 && g_tile_choice <= kNumTiles) return kTiles[g_tile_choice - 1];
@@ -996,7 +997,7 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   const qkn_launch_info info{name, grid, kThreads, grid * (kThreads / 64), lds};
   if (qkn_host::validate_only()) {
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, info.lds_bytes});
-    return QKN_OK;
+    return QKN_EDRYRUN;
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* args[] = {&p};

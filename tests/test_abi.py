@@ -1,8 +1,9 @@
 """The C ABI without a GPU: symbols, validation, overlap rules and path choice.
 
 Every call here either fails validation (which happens before any HIP call) or
-runs with the library's "validate_only" option set, which accepts the call and
-chooses a kernel without touching the GPU. The pointers are fake addresses that
+runs with the library's "validate_only" option set, which accepts the call,
+chooses a kernel without touching the GPU and returns QKN_EDRYRUN (never
+QKN_OK, so a call that launched nothing cannot pass for one that ran). The pointers are fake addresses that
 are never dereferenced, so these tests are safe on any machine.
 """
 import ctypes
@@ -18,6 +19,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 
 BASE = 0x7f0000000000  # fake, 256-byte aligned device addresses
 MB = 1 << 20
+DRY = L.QKN_EDRYRUN  # what a validated call returns under validate_only: nothing launched
 
 
 @pytest.fixture(scope="module")
@@ -77,18 +79,18 @@ def _k(T=64, d=256, rank_tp=4):
 
 
 def test_valid_calls_pass_validation(dry):
-    assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
+    assert _fused(dry, [_q(), _k()], 4, 1, 64) == DRY
     info = L.qkn_last_launch()
     assert info["kernel"].endswith("<2,1>/fused") and info["grid"] == 0
-    assert dry.qkn_partial_sumsq(BASE, 1024, 64, 1024, BASE + 64 * MB, None) == 0
+    assert dry.qkn_partial_sumsq(BASE, 1024, 64, 1024, BASE + 64 * MB, None) == DRY
     assert L.qkn_last_launch()["kernel"].endswith("<2,0>/partial")
     assert dry.qkn_apply(BASE, 1024, BASE + 64 * MB, BASE + 65 * MB, 4, 64, 1024, 4096,
-                         ctypes.c_float(1e-6), BASE + 128 * MB, 1024, None, None) == 0
+                         ctypes.c_float(1e-6), BASE + 128 * MB, 1024, None, None) == DRY
     assert L.qkn_last_launch()["kernel"].endswith("<2,0>/apply")
     full = [_seg(BASE, 4096, BASE + 64 * MB, 0, BASE + 128 * MB, 4096, 4096, 4096),
             _seg(BASE + 256 * MB, 1024, BASE + 300 * MB, 0, BASE + 400 * MB, 1024, 1024, 1024)]
     arr = (L.QknSeg * 2)(*full)
-    assert dry.qkn_full(arr, 2, 8192, ctypes.c_float(1e-6), None) == 0
+    assert dry.qkn_full(arr, 2, 8192, ctypes.c_float(1e-6), None) == DRY
     assert L.qkn_last_launch()["kernel"].endswith("<8,2>/fused")
 
 
@@ -99,7 +101,7 @@ def test_valid_calls_pass_validation(dry):
                                       (16392, "generic"), (100, "generic"), (1, "generic")])
 def test_path_choice_by_width(dry, d, expect):
     seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
-    assert _fused(dry, [seg], 2, 0, 16) == 0
+    assert _fused(dry, [seg], 2, 0, 16) == DRY
     name = L.qkn_last_launch()["kernel"]
     if expect in ("generic",) or expect.startswith("wide"):
         assert name.startswith(expect), name
@@ -110,29 +112,29 @@ def test_path_choice_by_width(dry, d, expect):
 def test_wide_path_needs_gamma_to_fit_lds(dry):
     q = _seg(BASE, 16384, BASE + 640 * MB, BASE + 641 * MB, BASE + 256 * MB, 16384, 16384, 16384)
     k = _seg(BASE + 512 * MB, 1024, BASE + 642 * MB, BASE + 643 * MB, BASE + 700 * MB, 1024, 1024, 1024)
-    assert _fused(dry, [q, k], 1, 0, 16) == 0   # 17408 gamma floats > 64 KiB of LDS
+    assert _fused(dry, [q, k], 1, 0, 16) == DRY   # 17408 gamma floats > 64 KiB of LDS
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
     q = _seg(BASE, 8192, BASE + 640 * MB, BASE + 641 * MB, BASE + 256 * MB, 8192, 8192, 8192)
-    assert _fused(dry, [q, k], 1, 0, 16) == 0
+    assert _fused(dry, [q, k], 1, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "wide<16,2>/fused"
     assert L.qkn_last_launch()["lds_bytes"] == (8192 + 1024) * 4
     # the wide tensor may come second: the launcher puts it in slot 0
-    assert _fused(dry, [k, q], 1, 0, 16) == 0
+    assert _fused(dry, [k, q], 1, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "wide<16,2>/fused"
     # both tensors wide: the general path
     k2 = _seg(BASE + 512 * MB, 5120, BASE + 642 * MB, BASE + 643 * MB, BASE + 700 * MB, 5120, 5120, 5120)
     q2 = _seg(BASE, 5120, BASE + 640 * MB, BASE + 641 * MB, BASE + 256 * MB, 5120, 5120, 5120)
-    assert _fused(dry, [q2, k2], 1, 0, 16) == 0
+    assert _fused(dry, [q2, k2], 1, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
 
 
 def test_prefetch_option_selects_variant(dry):
     seg = _seg(BASE, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 2048)
     assert dry.qkn_set_option(b"prefetch", 0) == 0
-    assert _fused(dry, [seg], 2, 0, 16) == 0
+    assert _fused(dry, [seg], 2, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows<2,0>/fused"
     assert dry.qkn_set_option(b"prefetch", 1) == 0
-    assert _fused(dry, [seg], 2, 0, 16) == 0
+    assert _fused(dry, [seg], 2, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pf<2,0>/fused"
     assert dry.qkn_set_option(b"prefetch", 2) == L.QKN_EINVAL
 
@@ -141,29 +143,29 @@ def test_register_path_needs_slot_offsets_in_range(dry):
     # tp * T * 4 bytes of statistics must stay below 2^31 for the register path
     G = 1 << 34  # regions of 16 GiB apart: x and y of 8M tokens x 1024 bf16 fit
     seg = _seg(BASE, 1024, BASE + 3 * G, BASE + 2 * G, BASE + G, 1024, 1024, 64 * 1024)
-    assert _fused(dry, [seg], 64, 0, (1 << 31) // (64 * 4)) == 0
+    assert _fused(dry, [seg], 64, 0, (1 << 31) // (64 * 4)) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
-    assert _fused(dry, [seg], 64, 0, (1 << 31) // (64 * 4) - 1) == 0
+    assert _fused(dry, [seg], 64, 0, (1 << 31) // (64 * 4) - 1) == DRY
     assert L.qkn_last_launch()["kernel"].startswith("rows")
 
 
 def test_path_choice_alignment_and_options(dry):
     # misaligned x (one element off) or a stride that is not a multiple of 8
     seg = _seg(BASE + 2, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 4096)
-    assert _fused(dry, [seg], 4, 0, 16) == 0
+    assert _fused(dry, [seg], 4, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
     seg = _seg(BASE, 1028, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 4096)
-    assert _fused(dry, [seg], 4, 0, 16) == 0
+    assert _fused(dry, [seg], 4, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
     seg = _seg(BASE, 1024, BASE + 64 * MB + 4, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 4096)
-    assert _fused(dry, [seg], 4, 0, 16) == 0
+    assert _fused(dry, [seg], 4, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
     # tp beyond one slot per lane
-    assert _fused(dry, [_q(rank_tp=65)], 65, 64, 16) == 0
+    assert _fused(dry, [_q(rank_tp=65)], 65, 64, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
     # forced general path
     assert dry.qkn_set_option(b"force_generic", 1) == 0
-    assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
+    assert _fused(dry, [_q(), _k()], 4, 1, 64) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic/fused"
     assert L.qkn_last_launch()["lds_bytes"] == 1024 * 2
 
@@ -236,7 +238,7 @@ def test_overlap_rules(dry):
     assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
     # exactly in place: allowed
     seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE, d, d, 2 * d)
-    assert _fused(dry, [seg], 2, 0, T) == 0
+    assert _fused(dry, [seg], 2, 0, T) == DRY
     # in place but a different stride: rejected
     seg = _seg(BASE, 2 * d, BASE + 64 * MB, BASE + 65 * MB, BASE, d, d, 2 * d)
     assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
@@ -244,7 +246,7 @@ def test_overlap_rules(dry):
     ld = 1024 + 256 + 256
     q = _seg(BASE, ld, BASE + 64 * MB, BASE + 65 * MB, BASE, ld, 1024, 4096)
     k = _seg(BASE + 2 * 1024, ld, BASE + 66 * MB, BASE + 67 * MB, BASE + 2 * 1024, ld, 256, 1024)
-    assert _fused(dry, [q, k], 4, 3, T) == 0
+    assert _fused(dry, [q, k], 4, 3, T) == DRY
     # K's output written over Q's input columns: rejected
     k = _seg(BASE + 2 * 1024, ld, BASE + 66 * MB, BASE + 67 * MB, BASE + 2 * 512, ld, 256, 1024)
     assert _fused(dry, [q, k], 4, 3, T) == L.QKN_EOVERLAP
@@ -255,7 +257,7 @@ def test_overlap_rules(dry):
     # ...but one array holding [2][tp][T] (disjoint per segment) is fine
     k = _seg(BASE + 256 * MB, 256, BASE + 300 * MB, BASE + 65 * MB + 2 * T * 4, BASE + 400 * MB,
              256, 256, 512)
-    assert _fused(dry, [q, k], 2, 0, T) == 0
+    assert _fused(dry, [q, k], 2, 0, T) == DRY
     # inv_rms over the partials array
     q = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d,
              inv=BASE + 65 * MB + 8)
@@ -264,7 +266,7 @@ def test_overlap_rules(dry):
     assert dry.qkn_partial_sumsq(BASE, d, T, d, BASE + 100, None) == L.QKN_EOVERLAP
     # y rows interleaved with x rows (same stride, column-disjoint): allowed
     seg = _seg(BASE, 2 * d, BASE + 64 * MB, BASE + 65 * MB, BASE + 2 * d, 2 * d, d, 2 * d)
-    assert _fused(dry, [seg], 2, 0, T) == 0
+    assert _fused(dry, [seg], 2, 0, T) == DRY
     # ...shifted by one column: overlaps
     seg = _seg(BASE, 2 * d, BASE + 64 * MB, BASE + 65 * MB, BASE + 2 * (d - 1), 2 * d, d, 2 * d)
     assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
@@ -349,7 +351,7 @@ def _k_nopart():
 
 def test_wait_entry_validation(dry):
     ok = _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block())
-    assert ok == 0
+    assert ok == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pa3<2,1>/fused_wait"  # publish three ahead
     for kw in (dict(epoch=0), dict(spin_limit=0), dict(co_resident=0), dict(status=None),
                dict(status=BASE + 700 * MB + 2), dict(slots=(None, BASE + 600 * MB)),
@@ -376,10 +378,10 @@ def test_wait_schedule_option(dry):
         for sched, prefix in ((0, "rows"), (1, "rows_pf"), (2, "rows_pa"), (3, "rows_pa2"),
                               (4, "rows_pa3")):
             assert dry.qkn_set_option(b"wait_schedule", sched) == 0
-            assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block()) == 0
+            assert _fused_wait(dry, [_q_nopart(), _k_nopart()], 4, 1, 64, _wait_block()) == DRY
             assert L.qkn_last_launch()["kernel"] == f"{prefix}<2,1>/fused_wait"
         # the option does not touch the kernels without a wait
-        assert _fused(dry, [_q(), _k()], 4, 1, 64) == 0
+        assert _fused(dry, [_q(), _k()], 4, 1, 64) == DRY
         assert L.qkn_last_launch()["kernel"] == "rows<2,1>/fused"
         assert dry.qkn_set_option(b"wait_schedule", 5) == L.QKN_EINVAL
         assert dry.qkn_set_option(b"wait_schedule", -1) == L.QKN_EINVAL
@@ -388,7 +390,7 @@ def test_wait_schedule_option(dry):
 
 
 def test_publish_entry_validation(dry):
-    assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == 0
+    assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows<2,0>/publish"
     assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB, 0, None) == L.QKN_EINVAL
     assert dry.qkn_publish_partials(BASE, 1024, 64, 1024, BASE + 512 * MB + 4, 7, None) == L.QKN_EINVAL
@@ -409,7 +411,7 @@ def test_group_entry_validation(dry):
         arr = (L.QknSeg * len(segs))(*segs)
         return dry.qkn_fused_group_wait(arr, len(segs), tp, T, ctypes.c_float(1e-6),
                                         ctypes.byref(wait), None)
-    assert call([full(1024, 4)], 4, _wait_block()) == 0
+    assert call([full(1024, 4)], 4, _wait_block()) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pa3<2,0>/fused_wait"
     bad = full(1024, 4)
     bad.d_full = 4000
@@ -438,7 +440,7 @@ def _fused8(lib, segs, tp, rank, T, eps=1e-6):
                                       (8, "generic_fp8"), (1000, "generic_fp8")])
 def test_fp8_path_choice_by_width(dry, d, expect):
     seg = _seg(BASE, d, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, d, d, 2 * d)
-    assert _fused8(dry, [seg], 2, 0, 16) == 0
+    assert _fused8(dry, [seg], 2, 0, 16) == DRY
     name = L.qkn_last_launch()["kernel"]
     assert name.startswith(expect + ("/" if expect.startswith("generic") else "")), name
 
@@ -446,21 +448,21 @@ def test_fp8_path_choice_by_width(dry, d, expect):
 def test_fp8_entry_points_validate_like_bf16(dry):
     q = _seg(BASE, 2048, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 2048, 2048, 4096)
     k = _seg(BASE + 256 * MB, 512, BASE + 300 * MB, BASE + 301 * MB, BASE + 400 * MB, 512, 512, 1024)
-    assert _fused8(dry, [q, k], 2, 1, 8192) == 0
+    assert _fused8(dry, [q, k], 2, 1, 8192) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,1>/fused"
-    assert dry.qkn_partial_sumsq_fp8(BASE, 2048, 64, 2048, BASE + 64 * MB, None) == 0
+    assert dry.qkn_partial_sumsq_fp8(BASE, 2048, 64, 2048, BASE + 64 * MB, None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,0>/partial"
     assert dry.qkn_apply_fp8(BASE, 2048, BASE + 64 * MB, BASE + 65 * MB, 2, 64, 2048, 4096,
-                             ctypes.c_float(1e-6), BASE + 128 * MB, 2048, None, None) == 0
+                             ctypes.c_float(1e-6), BASE + 128 * MB, 2048, None, None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,0>/apply"
     full = (L.QknSeg * 2)(_seg(BASE, 4096, BASE + 64 * MB, 0, BASE + 128 * MB, 4096, 4096, 4096),
                           _seg(BASE + 256 * MB, 1024, BASE + 300 * MB, 0, BASE + 400 * MB, 1024,
                                1024, 1024))
-    assert dry.qkn_full_fp8(full, 2, 8192, ctypes.c_float(1e-6), None) == 0
+    assert dry.qkn_full_fp8(full, 2, 8192, ctypes.c_float(1e-6), None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<4,1>/fused"
     # the prefetch option is a bf16-only variant; fp8 ignores it
     assert dry.qkn_set_option(b"prefetch", 1) == 0
-    assert _fused8(dry, [q, k], 2, 1, 8192) == 0
+    assert _fused8(dry, [q, k], 2, 1, 8192) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<2,1>/fused"
     # invalid arguments as for bf16
     assert _fused8(dry, [q, k], 2, 2, 64) == L.QKN_EINVAL
@@ -475,16 +477,16 @@ def test_fp8_entry_points_validate_like_bf16(dry):
 def test_fp8_alignment_and_overlap_in_bytes(dry):
     # a stride of 8 elements is 16-byte aligned for bf16 but not a whole fp8 chunk
     seg = _seg(BASE, 1032, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1032, 1024, 2048)
-    assert _fused8(dry, [seg], 2, 0, 16) == 0
+    assert _fused8(dry, [seg], 2, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic_fp8/fused"
     seg = _seg(BASE + 8, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 2048)
-    assert _fused8(dry, [seg], 2, 0, 16) == 0
+    assert _fused8(dry, [seg], 2, 0, 16) == DRY
     assert L.qkn_last_launch()["kernel"] == "generic_fp8/fused"
     # y directly after x (T rows of 1024 bytes) does not overlap; one byte earlier does
     T = 64
     x, y = BASE, BASE + T * 1024
     seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, y, 1024, 1024, 2048)
-    assert _fused8(dry, [seg], 2, 0, T) == 0
+    assert _fused8(dry, [seg], 2, 0, T) == DRY
     seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, y - 1, 1024, 1024, 2048)
     assert _fused8(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
     # the bf16 entry sees the same y overlapping (2-byte elements)
@@ -492,7 +494,7 @@ def test_fp8_alignment_and_overlap_in_bytes(dry):
     assert _fused(dry, [seg], 2, 0, T) == L.QKN_EOVERLAP
     # in place is allowed
     seg = _seg(x, 1024, BASE + 64 * MB, BASE + 65 * MB, x, 1024, 1024, 2048)
-    assert _fused8(dry, [seg], 2, 0, T) == 0
+    assert _fused8(dry, [seg], 2, 0, T) == DRY
 
 
 # ------------------------------------------------------------------ projection
@@ -568,7 +570,7 @@ def dry_proj_ok(lib, *args):
     """Validation passes: with validate_only the call returns before any HIP call."""
     assert lib.qkn_set_option(b"validate_only", 1) == 0
     try:
-        return _proj(lib, *args) == 0
+        return _proj(lib, *args) == DRY
     finally:
         assert lib.qkn_set_option(b"validate_only", 0) == 0
 
@@ -616,7 +618,7 @@ def test_proj_tile_option(lib):
 
 def test_calib_validation(dry):
     X, Y = BASE, BASE + 64 * MB
-    assert dry.qkn_calib_copy(X, Y, 1 << 20, 2048, None) == 0
+    assert dry.qkn_calib_copy(X, Y, 1 << 20, 2048, None) == DRY
     assert L.qkn_last_launch()["kernel"] == "calib_copy"
     assert dry.qkn_calib_copy(X, Y, 0, 2048, None) == 0                  # nothing to copy
     assert dry.qkn_calib_copy(X, Y, 24, 2048, None) == L.QKN_EINVAL      # not whole 16-byte vectors
@@ -626,7 +628,7 @@ def test_calib_validation(dry):
     assert dry.qkn_calib_copy(X + 8, Y, 1 << 20, 2048, None) == L.QKN_EINVAL
     assert dry.qkn_calib_copy(None, Y, 1 << 20, 2048, None) == L.QKN_EINVAL
     assert dry.qkn_calib_copy(X, X + (1 << 19), 1 << 20, 2048, None) == L.QKN_EOVERLAP
-    assert dry.qkn_calib_empty(None) == 0
+    assert dry.qkn_calib_empty(None) == DRY
     assert L.qkn_last_launch()["kernel"] == "calib_empty"
 
 
@@ -637,13 +639,13 @@ def test_fp8_wait_entries(dry):
     arr = (L.QknSeg * 2)(q, k)
     w = _wait_block()
     assert dry.qkn_fused_shard_wait_fp8(arr, 2, 4, 1, 64, ctypes.c_float(1e-6), ctypes.byref(w),
-                                        None) == 0
+                                        None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pa3_fp8<1,1>/fused_wait"
-    assert dry.qkn_publish_partials_fp8(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == 0
+    assert dry.qkn_publish_partials_fp8(BASE, 1024, 64, 1024, BASE + 512 * MB, 7, None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_fp8<1,0>/publish"
     full = (L.QknSeg * 1)(_seg(BASE, 4096, BASE + 64 * MB, None, BASE + 128 * MB, 4096, 1024, 4096))
     assert dry.qkn_fused_group_wait_fp8(full, 1, 4, 64, ctypes.c_float(1e-6), ctypes.byref(w),
-                                        None) == 0
+                                        None) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pa3_fp8<1,0>/fused_wait"
     # the register path's limits are in bytes: 8 codes per row are not a 16-byte chunk
     odd = (L.QknSeg * 1)(_seg(BASE, 1032, BASE + 64 * MB, None, BASE + 128 * MB, 1032, 1032, 4128))
@@ -675,8 +677,67 @@ def test_proj_size_limits(lib):
 def test_wait_schedule_capped_for_the_widest_rows(dry):
     q = _seg(BASE, 4096, BASE + 64 * MB, None, BASE + 128 * MB, 4096, 4096, 8192)
     k = _seg(BASE + 256 * MB, 4096, BASE + 300 * MB, None, BASE + 400 * MB, 4096, 4096, 8192)
-    assert _fused_wait(dry, [q, k], 2, 1, 64, _wait_block()) == 0
+    assert _fused_wait(dry, [q, k], 2, 1, 64, _wait_block()) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pf<8,8>/fused_wait"
     k2 = _seg(BASE + 256 * MB, 2048, BASE + 300 * MB, None, BASE + 400 * MB, 2048, 2048, 4096)
-    assert _fused_wait(dry, [q, k2], 2, 1, 64, _wait_block()) == 0
+    assert _fused_wait(dry, [q, k2], 2, 1, 64, _wait_block()) == DRY
     assert L.qkn_last_launch()["kernel"] == "rows_pa3<8,4>/fused_wait"
+
+
+def test_spin_limit_is_capped(dry):
+    """A wait stays bounded whatever the caller asks: spin_limit above
+    QKN_MAX_SPIN_LIMIT (2^22 polls) is rejected before anything is launched."""
+    cap = 1 << 22
+    segs = [_q_nopart(), _k_nopart()]
+    assert _fused_wait(dry, segs, 4, 1, 64, _wait_block(spin_limit=cap)) == DRY
+    assert _fused_wait(dry, segs, 4, 1, 64, _wait_block(spin_limit=cap + 1)) == L.QKN_EINVAL
+    assert _fused_wait(dry, segs, 4, 1, 64, _wait_block(spin_limit=1 << 62)) == L.QKN_EINVAL
+    full = (L.QknSeg * 1)(_seg(BASE, 4096, BASE + 64 * MB, None, BASE + 128 * MB, 4096, 1024, 4096))
+    assert dry.qkn_fused_group_wait(full, 1, 4, 64, ctypes.c_float(1e-6),
+                                    ctypes.byref(_wait_block(spin_limit=cap + 1)), None) == \
+        L.QKN_EINVAL
+
+
+def test_wait_slot_offsets_in_range(dry):
+    """Flagged slots are 8 bytes: the waiting kernel addresses a token's slots
+    by 32-bit byte offsets, so tp * T * 8 must stay below 2^31 (else
+    QKN_ENOTSUP, never a launch whose offsets wrap)."""
+    G = 1 << 38  # regions 256 GiB apart: x, y (128 GiB each) and the slot arrays fit
+    tp = 4
+    q = _seg(BASE, 1024, BASE + 3 * G, None, BASE + G, 1024, 1024, 4096)
+    limit = (1 << 31) // (tp * 8)  # 2^26 tokens: tp * T = 2^28
+    for T, expect in ((limit - 1, DRY), (limit, L.QKN_ENOTSUP)):
+        w = _wait_block(slots=(BASE + 4 * G, BASE + 5 * G), status=BASE + 6 * G)
+        assert _fused_wait(dry, [q], tp, 1, T, w) == expect, T
+    # the statistics of the kernels without a wait are 4 bytes: twice the tokens
+    qp = _seg(BASE, 1024, BASE + 3 * G, BASE + 4 * G, BASE + G, 1024, 1024, 4096)
+    assert _fused(dry, [qp], tp, 1, limit) == DRY
+    assert L.qkn_last_launch()["kernel"].startswith("rows")
+
+
+def test_options_are_per_thread(lib):
+    """A setting made in one thread does not reach another thread's launches:
+    validate_only set here leaves a worker thread's calls launching normally
+    (checked on validation-failing-free calls that stop at the first HIP query
+    on this CPU-only machine), and a worker's settings do not come back."""
+    import threading
+    seg = _seg(BASE, 1024, BASE + 64 * MB, BASE + 65 * MB, BASE + 128 * MB, 1024, 1024, 2048)
+    got = {}
+
+    def worker():
+        # no validate_only in this thread: the call goes on to the HIP runtime,
+        # which has no device here (QKN_EHIP) -- or launches, where there is one
+        got["rc"] = _fused(lib, [seg], 2, 0, 16)
+        got["prefetch"] = lib.qkn_set_option(b"prefetch", 1)
+
+    assert lib.qkn_set_option(b"validate_only", 1) == 0
+    try:
+        th = threading.Thread(target=worker)
+        th.start()
+        th.join()
+        assert got["rc"] != DRY and got["prefetch"] == 0
+        # this thread: still validate_only, and the worker's prefetch setting did not leak
+        assert _fused(lib, [seg], 2, 0, 16) == DRY
+        assert L.qkn_last_launch()["kernel"] == "rows<2,0>/fused"
+    finally:
+        assert lib.qkn_set_option(b"validate_only", 0) == 0

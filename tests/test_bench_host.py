@@ -29,14 +29,21 @@ def test_profiler_names():
         "qkn_calib_copy_kernel"
 
 
-def test_counter_summary_is_used_only_for_the_current_source():
+def test_counter_summary_is_used_only_for_the_current_source(monkeypatch):
     wl = workloads.PREFILL_TP2
     path = bench.counters_path("rows<4,1>/fused", wl.name)
     assert os.path.basename(path) == f"counters_rows_4_1_fused_{wl.name}.txt"
     text = open(path).read()
-    assert f"source_sha256: {bench.source_sha256()}" in text, "profiles/ predate the kernel source"
-    assert bench.traffic_bytes("rows<4,1>/fused", wl.name) > bench.algorithmic_bytes(
-        wl.T, (wl.q_local, wl.k_local), wl.tp)
+    alg = bench.algorithmic_bytes(wl.T, (wl.q_local, wl.k_local), wl.tp)
+    if f"source_sha256: {bench.source_sha256()}" in text:
+        # counters of the current source: used, and at least the algorithmic bytes
+        assert bench.traffic_bytes("rows<4,1>/fused", wl.name) > alg
+    else:
+        # taken before the last kernel change: not used
+        assert bench.traffic_bytes("rows<4,1>/fused", wl.name) is None
+    # a summary whose recorded hash differs from the source is never used
+    monkeypatch.setattr(bench, "source_sha256", lambda: "0" * 64)
+    assert bench.traffic_bytes("rows<4,1>/fused", wl.name) is None
 
 
 def test_every_launch_name_family_maps():

@@ -22,7 +22,8 @@ from oracle import compare
 from oracle import qknorm as Q
 from paper_2608_09160_amd import _lib as L
 
-from gpu_util import DEV, bits_of, inputs, peer_partials, run_fused_rank, shard, to_dev_f32, to_dev_fp8
+from gpu_util import (DEV, bits_of, check_ranks_every_token, inputs, peer_partials, run_fused_rank,
+                      shard, to_dev_f32, to_dev_fp8)
 
 pytestmark = pytest.mark.gpu
 
@@ -248,25 +249,28 @@ def test_fp8_zero_tokens_and_dtype_errors():
     assert e.value.status == L.QKN_EOVERLAP
 
 
-def test_fp8_full_size_sampled():
-    """The FP8 prefill shard at its full token count in the benchmark's launch shape."""
-    wl = workloads.PREFILL_TP2.with_dtype("fp8")
+@pytest.mark.parametrize("wl,kernel", [
+    (workloads.PREFILL_TP2.with_dtype("fp8"), "rows_fp8<2,1>/fused"),
+    (workloads.LONG_PREFILL_TP4.with_dtype("fp8"), "rows_fp8<2,1>/fused")],
+    ids=lambda v: getattr(v, "name", v))
+def test_fp8_full_size_every_token(wl, kernel):
+    """The FP8 prefill shards at their full token counts in the benchmark's
+    launch shape (several tokens per wavefront): every rank and every token
+    against the oracle; own statistic == Phase A alone; a second launch gives
+    the same bits."""
     data = inputs(wl)
-    rank = 1
-    print(f"[fp8] full size {wl.name} rank {rank}", flush=True)
-    out = run_fused_rank(wl, data, rank)
-    assert out["launch"]["kernel"] == "rows_fp8<2,1>/fused"
-    rng = np.random.default_rng(12)
-    rows = np.unique(np.concatenate([[0, 1, wl.T - 1], rng.choice(wl.T, 253, replace=False)]))
-    sub = {k: (v[rows] if v.ndim == 2 else v) for k, v in data.items()}
-    ref = _ref(wl, sub, wl.tp, rank)
-    for t, key, d_full in (("q", "xq", wl.q_full), ("k", "xk", wl.k_full)):
-        compare.check_fp8(Q.decode_e4m3(out[t]["y"][rows]), ref[t]["y"], f"{t} sampled y")
-        compare.check_close(out[t]["partials"][rank][rows], ref[t]["partials"][rank],
-                            compare.PARTIAL_RTOL, f"{t} sampled partial")
-        assert not np.isnan(Q.decode_e4m3(out[t]["y"])).any()
-        alone = L.qkn_partial_sumsq_fp8(to_dev_fp8(shard(data, key, d_full, wl.tp, rank)))
-        assert np.array_equal(out[t]["partials"][rank], alone.cpu().numpy())
-    again = run_fused_rank(wl, data, rank)
+    outs = {}
+    for rank in range(wl.tp):
+        print(f"[fp8] full size {wl.name} rank {rank}", flush=True)
+        out = run_fused_rank(wl, data, rank)
+        assert out["launch"]["kernel"] == kernel and out["launch"]["waves"] < wl.T
+        for t, key, d_full in (("q", "xq", wl.q_full), ("k", "xk", wl.k_full)):
+            assert not np.isnan(Q.decode_e4m3(out[t]["y"])).any()
+            alone = L.qkn_partial_sumsq_fp8(to_dev_fp8(shard(data, key, d_full, wl.tp, rank)))
+            assert np.array_equal(out[t]["partials"][rank], alone.cpu().numpy())
+        outs[rank] = out
+    print(f"[fp8] oracle on every token: {wl.name}", flush=True)
+    check_ranks_every_token(wl, data, outs, wl.name)
+    again = run_fused_rank(wl, data, 0)
     for t in "qk":
-        assert np.array_equal(again[t]["y"], out[t]["y"])
+        assert np.array_equal(again[t]["y"], outs[0][t]["y"])

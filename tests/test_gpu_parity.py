@@ -17,8 +17,8 @@ from oracle import compare
 from oracle import qknorm as Q
 from paper_2608_09160_amd import _lib as L
 
-from gpu_util import (DEV, bits_of, inputs, peer_partials, run_fused_rank, shard, to_dev_bf16,
-                      to_dev_f32)
+from gpu_util import (DEV, bits_of, check_rank_every_token, check_ranks_every_token, inputs,
+                      peer_partials, run_fused_rank, shard, to_dev_bf16, to_dev_f32)
 
 pytestmark = pytest.mark.gpu
 
@@ -182,48 +182,66 @@ def test_phase_c_rounding_is_rne_of_fp32_product():
 
 @pytest.mark.parametrize("wl", [workloads.PREFILL_TP2, workloads.LONG_PREFILL_TP4],
                          ids=lambda w: w.name)
-def test_full_size_sampled(wl):
-    """Full token counts in the benchmark's launch shape; the oracle checks a
-    sample of tokens one by one, properties are checked on every token."""
+def test_full_size_every_token(wl):
+    """Full token counts in the benchmark's launch shape (each wavefront walks
+    several tokens of the persistent loop): every rank, every token, every
+    element against the oracle; own statistic == Phase A alone; equal factors
+    on all ranks; a second launch gives the same bits."""
     data = inputs(wl)
-    rank = wl.tp - 1
-    print(f"[parity] full size {wl.name} rank {rank}", flush=True)
-    out = run_fused_rank(wl, data, rank)
-    assert out["launch"]["kernel"].startswith("rows")
-    rng = np.random.default_rng(11)
-    rows = np.unique(np.concatenate([[0, 1, wl.T - 1], rng.choice(wl.T, 253, replace=False)]))
-    sub = {k: (v[rows] if v.ndim == 2 else v) for k, v in data.items()}
-    ref = Q.qknorm_layerwise(sub["xq"], sub["xk"], sub["gq"], sub["gk"], wl.tp, rank, wl.eps)
+    outs = {}
+    for rank in range(wl.tp):
+        print(f"[parity] full size {wl.name} rank {rank}", flush=True)
+        out = run_fused_rank(wl, data, rank)
+        assert out["launch"]["kernel"].startswith("rows")
+        assert out["launch"]["waves"] < wl.T  # several tokens per wavefront
+        outs[rank] = out
+    print(f"[parity] oracle on every token: {wl.name}", flush=True)
+    check_ranks_every_token(wl, data, outs, wl.name)
+    for rank, out in outs.items():
+        for t, key, d_full in (("q", "xq", wl.q_full), ("k", "xk", wl.k_full)):
+            alone = L.qkn_partial_sumsq(to_dev_bf16(shard(data, key, d_full, wl.tp, rank)))
+            assert np.array_equal(out[t]["partials"][rank], alone.cpu().numpy())
+            assert np.array_equal(out[t]["inv"], outs[0][t]["inv"])
+    again = run_fused_rank(wl, data, wl.tp - 1)
     for t in "qk":
-        compare.check_close(Q.decode_bf16(out[t]["y"][rows]), ref[t]["y"], compare.OUTPUT_RTOL,
-                            f"{t} sampled y")
-        compare.check_close(out[t]["partials"][rank][rows], ref[t]["partials"][rank],
-                            compare.PARTIAL_RTOL, f"{t} sampled partial")
-        assert np.isfinite(Q.decode_bf16(out[t]["y"])).all()
-    # every token: own statistic == Phase A alone; rank 0 sees the same factors
-    for t, key, d_full in (("q", "xq", wl.q_full), ("k", "xk", wl.k_full)):
-        alone = L.qkn_partial_sumsq(to_dev_bf16(shard(data, key, d_full, wl.tp, rank)))
-        assert np.array_equal(out[t]["partials"][rank], alone.cpu().numpy())
-    out0 = run_fused_rank(wl, data, 0)
-    for t in "qk":
-        assert np.array_equal(out0[t]["inv"], out[t]["inv"])
-    # determinism: a second launch gives the same bits
-    again = run_fused_rank(wl, data, rank)
-    for t in "qk":
-        assert np.array_equal(again[t]["y"], out[t]["y"])
+        assert np.array_equal(again[t]["y"], outs[wl.tp - 1][t]["y"])
 
 
-def test_full_vector_prefill_sampled():
+def test_full_vector_prefill_every_token():
+    """The tp = 1 baseline (the compute of the all-gather path) at 8192 tokens:
+    every token against the oracle."""
     wl = workloads.PREFILL_TP2.with_tp(1)
     data = inputs(workloads.PREFILL_TP2)
     print("[parity] full-vector prefill", flush=True)
     out = run_fused_rank(wl, data, 0)
     assert out["launch"]["kernel"].endswith("<8,2>/fused")
-    rows = np.arange(0, wl.T, 37)
-    sub = {k: (v[rows] if v.ndim == 2 else v) for k, v in data.items()}
-    ref = Q.qknorm_layerwise(sub["xq"], sub["xk"], sub["gq"], sub["gk"], 1, 0, wl.eps)
-    for t in "qk":
-        compare.check_close(Q.decode_bf16(out[t]["y"][rows]), ref[t]["y"], compare.OUTPUT_RTOL, t)
+    assert out["launch"]["waves"] < wl.T
+    check_rank_every_token(wl, data, 0, out, wl.name)
+
+
+@pytest.mark.parametrize("opt", [None, ("waves_per_cu", 1), ("prefetch", 1), ("balance", 1),
+                                 ("token_blocks", 1), ("waves_per_block", 4)],
+                         ids=lambda o: "default" if o is None else f"{o[0]}={o[1]}")
+def test_several_tokens_per_wave_against_oracle(opt):
+    """A ragged token count (2049) with one wavefront per CU, so every
+    wavefront walks eight or nine tokens of the persistent loop, under each
+    scheduling option (strided tokens, the pipelined loop, equal shares,
+    contiguous blocks): every token against the oracle."""
+    wl = workloads.PREFILL_TP2.with_tokens(2049)
+    data = inputs(wl)
+    opts = [("waves_per_cu", 1)] if opt is None or opt[0] != "waves_per_cu" else []
+    if opt is not None:
+        opts.append(opt)
+    for k, v in opts:
+        L.qkn_set_option(k, v)
+    try:
+        out = run_fused_rank(wl, data, 1)
+    finally:
+        for k, _ in opts:
+            L.qkn_set_option(k, 0)
+    waves = out["launch"]["waves"]
+    assert waves * 8 <= wl.T, out["launch"]
+    check_rank_every_token(wl, data, 1, out, f"{wl.name} {opts}")
 
 
 # ------------------------------------------------------------------ general path and shapes
