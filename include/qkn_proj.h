@@ -98,6 +98,35 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
                      const qkn_proj_seg* segs, int nseg, void* workspace,
                      int64_t workspace_bytes, void* stream);
 
+/*
+ * Size of the fixed device workspace of qkn_proj_partial_noalloc: 32 MiB,
+ * held on each GPU the entry point runs on from its first call there until
+ * the process ends. It covers every decode-sized (split-k) launch of up to
+ * 4096 output columns over Q and K together (the split workspace is at most
+ * 4 * 2048 * columns bytes) and the chunk statistics of prefill launches up to
+ * T * sum of ceil(d_local / 128) = 8 M.
+ */
+#define QKN_PROJ_SCRATCH_BYTES (INT64_C(32) << 20)
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * computation, kernels and results (bit for bit) as qkn_proj_partial, with the
+ * workspace taken from a fixed per-device array of QKN_PROJ_SCRATCH_BYTES
+ * instead of an argument. It calls no allocator (no hipMalloc, no hipFree);
+ * its first call on a device looks the array's address up once (a runtime
+ * query, no allocation). Every call on one GPU shares that GPU's array, which
+ * keeps the last call's contents (no call needs it cleared: every workspace
+ * byte a call's kernels read was written earlier by the same call's kernels,
+ * in stream order); calls that overlap in time on
+ * one GPU -- on different streams, or from different threads -- race on it
+ * and must be ordered by the caller.
+ * Status codes as qkn_proj_partial, and QKN_ENOTSUP when the launch needs more
+ * than QKN_PROJ_SCRATCH_BYTES (qkn_proj_workspace_bytes tells how much).
+ */
+int qkn_proj_partial_noalloc(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
+                             const qkn_proj_seg* segs, int nseg, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,6 +24,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqkn.so")
 
 QKN_OK, QKN_EINVAL, QKN_EOVERLAP, QKN_EHIP, QKN_ENOTSUP, QKN_EDRYRUN = 0, -1, -2, -3, -4, -5
+QKN_PROJ_SCRATCH_BYTES = 32 << 20  # include/qkn_proj.h: qkn_proj_partial_noalloc's fixed workspace
 
 _c_i64 = ctypes.c_int64
 _vp = ctypes.c_void_p
@@ -91,6 +92,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qkn_proj_workspace_bytes.restype = _c_i64
     lib.qkn_proj_partial.argtypes = [_vp, _c_i64, _c_i64, _c_i64, ctypes.POINTER(QknProjSeg),
                                      ctypes.c_int, _vp, _c_i64, _vp]
+    lib.qkn_proj_partial_noalloc.argtypes = [_vp, _c_i64, _c_i64, _c_i64,
+                                             ctypes.POINTER(QknProjSeg), ctypes.c_int, _vp]
     lib.qkn_calib_copy.argtypes = [_vp, _vp, _c_i64, _c_i64, _vp]
     lib.qkn_calib_empty.argtypes = [_vp]
     lib.qkn_strerror.argtypes = [ctypes.c_int]
@@ -101,6 +104,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                  "qkn_last_launch", "qkn_set_option", "qkn_publish_partials",
                  "qkn_fused_shard_wait", "qkn_fused_group_wait", "qkn_partial_sumsq_fp8",
                  "qkn_apply_fp8", "qkn_fused_shard_fp8", "qkn_full_fp8", "qkn_proj_partial",
+                 "qkn_proj_partial_noalloc",
                  "qkn_calib_copy", "qkn_calib_empty", "qkn_publish_partials_fp8",
                  "qkn_fused_shard_wait_fp8", "qkn_fused_group_wait_fp8"):
         getattr(lib, name).restype = ctypes.c_int
@@ -490,6 +494,18 @@ def qkn_proj_partial(x: torch.Tensor, segs: Sequence[ProjSeg],
         raise ValueError("workspace: expected a contiguous uint8 GPU tensor")
     _check(load().qkn_proj_partial(px, ldx, T, hidden, arr, len(segs), workspace.data_ptr(),
                                    workspace.numel(), _stream(stream)), "qkn_proj_partial")
+    return [(s.y, s.partials) for s in segs]
+
+
+def qkn_proj_partial_noalloc(x: torch.Tensor, segs: Sequence[ProjSeg], stream=None):
+    """qkn_proj_partial with the library's fixed per-device workspace instead
+    of a caller's one (the entry point allocates nothing; the segments' y and
+    partials must be given if this call may not allocate either). Returns the
+    segments' (y, partials) pairs."""
+    px, ldx, T, hidden = _rows(x, "x")
+    arr = _proj_segs(segs, T, hidden, x.device)
+    _check(load().qkn_proj_partial_noalloc(px, ldx, T, hidden, arr, len(segs), _stream(stream)),
+           "qkn_proj_partial_noalloc")
     return [(s.y, s.partials) for s in segs]
 
 

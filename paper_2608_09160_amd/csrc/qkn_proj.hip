@@ -53,6 +53,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "qkn_proj.h"
 #include "qkn_host.h"
 
@@ -865,28 +867,42 @@ Plan plan_of(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg) {
   return pl;
 }
 
-}  // namespace
+// ---------------------------------------------------------------- workspace without allocation
+//
+// The entry point for callers that cannot allocate (HIP graph capture, tight
+// serving loops) takes its workspace from this fixed device array instead of
+// an argument. Each GPU the library runs on holds its own copy, from the
+// first such call until the process ends. Host code never passes the array's
+// name to a kernel or a copy (on the host that name is a stand-in, not a
+// device address): it asks the runtime for the array's address on each device
+// once, with that device current, and passes that address.
+constexpr int64_t kScratchBytes = QKN_PROJ_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
-namespace qkn_host {
-int set_proj_tile(int64_t choice) {
-  if (choice < 0 || choice > kNumTiles) return QKN_EINVAL;
-  g_tile_choice = static_cast<int>(choice);
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The current device's address of `scratch`, looked up on its first use.
+int scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return QKN_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return QKN_EHIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
   return QKN_OK;
 }
-}  // namespace qkn_host
 
-extern "C" {
-
-int64_t qkn_proj_workspace_bytes(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg) {
-  if (!segs || nseg < 1 || nseg > 2 || T < 0 || hidden < 1) return QKN_EINVAL;
-  for (int i = 0; i < nseg; ++i)
-    if (segs[i].d_local < 1) return QKN_EINVAL;
-  return plan_of(T, hidden, segs, nseg).ws_bytes;
-}
-
-int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
-                     const qkn_proj_seg* segs, int nseg, void* workspace,
-                     int64_t workspace_bytes, void* stream) {
+// qkn_proj_partial's body. use_scratch: the workspace is `scratch` (its
+// address resolved only once the call is valid and about to launch), and
+// `workspace` / `workspace_bytes` are ignored.
+int proj_impl(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
+              const qkn_proj_seg* segs, int nseg, void* workspace, int64_t workspace_bytes,
+              bool use_scratch, void* stream) {
   if (!segs || nseg < 1 || nseg > 2 || T < 0 || hidden < 1 || ldx < hidden) return QKN_EINVAL;
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
@@ -898,12 +914,16 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     if (!segs[i].w || !segs[i].y || !segs[i].partials) return QKN_EINVAL;
   const Plan pl = plan_of(T, hidden, segs, nseg);
   const int64_t need = pl.ws_bytes;
-  if (!workspace || workspace_bytes < need) return QKN_EINVAL;
+  if (use_scratch) {
+    if (need > kScratchBytes) return QKN_ENOTSUP;  // beyond the fixed workspace
+  } else if (!workspace || workspace_bytes < need) {
+    return QKN_EINVAL;
+  }
 
   // the MFMA path's shape and alignment requirements
   const int64_t lim = int64_t{1} << 31;
-  if (!aligned16(x) || !aligned16(workspace) || hidden % 8 || ldx % 8 || T * ldx * 2 >= lim ||
-      hidden > (int64_t{1} << 30))
+  if (!aligned16(x) || (!use_scratch && !aligned16(workspace)) || hidden % 8 || ldx % 8 ||
+      T * ldx * 2 >= lim || hidden > (int64_t{1} << 30))
     return QKN_ENOTSUP;
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
@@ -912,14 +932,16 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
       return QKN_ENOTSUP;
   }
 
-  // overlap: outputs (y, partials, workspace) against inputs and each other
+  // overlap: outputs (y, partials, a caller's workspace) against inputs and each other
   Span items[8];
   bool out[8];
   int n = 0;
   items[n] = Span{reinterpret_cast<uintptr_t>(x), T, ldx, hidden, 2};
   out[n++] = false;
-  items[n] = Span{reinterpret_cast<uintptr_t>(workspace), 1, need, need, 1};
-  out[n++] = true;
+  if (!use_scratch) {
+    items[n] = Span{reinterpret_cast<uintptr_t>(workspace), 1, need, need, 1};
+    out[n++] = true;
+  }
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
     items[n] = Span{reinterpret_cast<uintptr_t>(s.w), s.d_local, s.ldw, hidden, 2};
@@ -946,9 +968,9 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   p.splits = pl.splits;
   p.kslice = pl.kslice;
   p.ncols = static_cast<int32_t>(pl.ncols);
-  float* ws = static_cast<float*>(workspace);
-  p.part = split ? ws : nullptr;
+  int64_t ws_off[2] = {0, 0};  // floats into the workspace of each segment's chunk statistics
   int32_t tile0 = 0, col0 = 0;
+  int64_t off = 0;
   for (int i = 0; i < nseg; ++i) {
     const qkn_proj_seg& s = segs[i];
     ProjSegDev& d = p.seg[i];
@@ -961,8 +983,8 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     d.tile0 = tile0;
     d.col0 = col0;
     d.nchunks = static_cast<int32_t>(chunks_of(s.d_local));
-    d.tile_partials = split ? nullptr : ws;
-    if (!split) ws += static_cast<int64_t>(d.nchunks) * T;
+    ws_off[i] = off;
+    if (!split) off += static_cast<int64_t>(d.nchunks) * T;
     tile0 += static_cast<int32_t>((s.d_local + 127) / 128);  // every kernel's tiles are 128 wide
     col0 += static_cast<int32_t>(s.d_local);
   }
@@ -999,6 +1021,13 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
     qkn_host::record_launch(qkn_launch_info{info.kernel, 0, 0, 0, info.lds_bytes});
     return QKN_EDRYRUN;
   }
+  if (use_scratch) {
+    const int rc = scratch_address(&workspace);
+    if (rc != QKN_OK) return rc;
+  }
+  float* ws = static_cast<float*>(workspace);
+  p.part = split ? ws : nullptr;
+  for (int i = 0; i < nseg; ++i) p.seg[i].tile_partials = split ? nullptr : ws + ws_off[i];
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* args[] = {&p};
   if (hipLaunchKernel(gemm, dim3(static_cast<unsigned>(grid)), dim3(kThreads), args, 0, st) !=
@@ -1023,6 +1052,36 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
   }
   qkn_host::record_launch(info);
   return QKN_OK;
+}
+
+}  // namespace
+
+namespace qkn_host {
+int set_proj_tile(int64_t choice) {
+  if (choice < 0 || choice > kNumTiles) return QKN_EINVAL;
+  g_tile_choice = static_cast<int>(choice);
+  return QKN_OK;
+}
+}  // namespace qkn_host
+
+extern "C" {
+
+int64_t qkn_proj_workspace_bytes(int64_t T, int64_t hidden, const qkn_proj_seg* segs, int nseg) {
+  if (!segs || nseg < 1 || nseg > 2 || T < 0 || hidden < 1) return QKN_EINVAL;
+  for (int i = 0; i < nseg; ++i)
+    if (segs[i].d_local < 1) return QKN_EINVAL;
+  return plan_of(T, hidden, segs, nseg).ws_bytes;
+}
+
+int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
+                     const qkn_proj_seg* segs, int nseg, void* workspace,
+                     int64_t workspace_bytes, void* stream) {
+  return proj_impl(x, ldx, T, hidden, segs, nseg, workspace, workspace_bytes, false, stream);
+}
+
+int qkn_proj_partial_noalloc(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
+                             const qkn_proj_seg* segs, int nseg, void* stream) {
+  return proj_impl(x, ldx, T, hidden, segs, nseg, nullptr, 0, true, stream);
 }
 
 }  // extern "C"

@@ -741,3 +741,30 @@ def test_options_are_per_thread(lib):
         assert L.qkn_last_launch()["kernel"] == "rows<2,0>/fused"
     finally:
         assert lib.qkn_set_option(b"validate_only", 0) == 0
+
+
+def test_proj_noalloc_validation(dry):
+    """qkn_proj_partial_noalloc: the projection's checks, and a launch whose
+    workspace exceeds the fixed QKN_PROJ_SCRATCH_BYTES (32 MiB) is rejected
+    with QKN_ENOTSUP before any HIP call."""
+    X, W, Y, P = BASE, BASE + 64 * MB, BASE + 1024 * MB, BASE + 2048 * MB
+
+    def call(T, h, dims, x=X):
+        segs = [_pseg(W + i * 256 * MB, h, Y + i * 256 * MB, d, P + i * MB, d)
+                for i, d in enumerate(dims)]
+        arr = (L.QknProjSeg * len(segs))(*segs)
+        need = dry.qkn_proj_workspace_bytes(T, h, arr, len(segs))
+        return dry.qkn_proj_partial_noalloc(x, h, T, h, arr, len(segs), None), need
+
+    assert L.QKN_PROJ_SCRATCH_BYTES == 32 << 20
+    rc, need = call(64, 4096, (1024, 256))   # decode: split-k slice sums, 5 MiB
+    assert rc == DRY and need == 4 * 16 * 64 * 1280
+    assert L.qkn_last_launch()["kernel"] == "proj<64x128,64,dl4,splitk>"
+    rc, need = call(8192, 4096, (2048, 512))  # prefill: chunk statistics
+    assert rc == DRY and L.qkn_last_launch()["kernel"] == "proj<128x128,64,dl2,mi16>"
+    rc, need = call(1024, 4096, (4096, 1024))  # two slices over 5120 columns: 40 MiB
+    assert need > L.QKN_PROJ_SCRATCH_BYTES and rc == L.QKN_ENOTSUP
+    rc, _ = call(64, 4096, (1024, 256), x=None)
+    assert rc == L.QKN_EINVAL
+    rc, _ = call(0, 4096, (1024, 256), x=None)  # nothing to do
+    assert rc == L.QKN_OK
