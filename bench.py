@@ -29,6 +29,12 @@ import platform
 import sys
 import time
 
+if __name__ == "__main__":
+    # the oracle's CPU baseline runs on one host thread: pin the thread pools
+    # of numpy's libraries before numpy is imported
+    for _var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[_var] = "1"
+
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
@@ -56,6 +62,16 @@ def parse():
     p.add_argument("--summarize-proj", metavar="DIR",
                    help="write profiles/counters_proj_*.txt from rocprofv3 --pmc CSV output of "
                         "`bench.py --proj-only` in DIR/pmc_proj1 and DIR/pmc_proj2")
+    p.add_argument("--counter-pass", action="store_true",
+                   help="launch every kernel family measured in profiles/ (the headline, the "
+                        "two-launch baseline, the group wait, tp = 1, the long shard, FP8, the "
+                        "projection) a fixed number of times between marker launches and print "
+                        "their list as JSON: the program that the rocprofv3 --pmc passes of "
+                        "--summarize-counters profile")
+    p.add_argument("--summarize-counters", metavar="DIR",
+                   help="write profiles/counters_*.txt and profiles/issue_rate_*.md from the "
+                        "rocprofv3 --pmc output of `bench.py --counter-pass` in DIR/<pass> "
+                        "(one directory per entry of COUNTER_PASSES) and DIR/counter_pass.json")
     p.add_argument("--calibration-copy", action="store_true",
                    help="also run a plain device copy of Q's input (known bytes) a few times, "
                         "to scale profiler byte counters")
@@ -260,6 +276,48 @@ def stream_copy_ms(torch, L, nbytes: int, min_footprint: int, steps: int, warmup
     return best
 
 
+def token_fit(torch, L, min_fp: int, steps: int, warmup: int,
+              tokens=(2048, 4096, 8192, 16384, 32768), widths=(2048, 512), tp=2):
+    """Launch time of the fused kernel against the token count at the prefill
+    shard's widths (Q 2048 + K 512 per rank, tp 2), cold (rotating buffer sets
+    of >= min_fp bytes, device-random bf16 rows), and a least-squares line
+    time = intercept + slope * T; the same for the streaming copy of the same
+    bytes. The intercept is the fixed cost per launch, the slope the streaming
+    rate."""
+    dev = "cuda:0"
+    pts, cps = [], []
+    for T in tokens:
+        nbytes = algorithmic_bytes(T, widths, tp)
+        set_bytes = sum(2 * T * d * 2 for d in widths)  # x read + y written
+        nsets = max(2, -(-min_fp // set_bytes))
+        calls = []
+        for _ in range(nsets):
+            segs = []
+            for d in widths:
+                x = torch.randn((T, d), device=dev).to(torch.bfloat16)
+                P = torch.rand((tp, T), device=dev) + 0.5
+                segs.append(L.Seg(x=x, w=torch.rand(d, device=dev) + 0.5, d_full=d * tp,
+                                  y=torch.empty_like(x), partials=P))
+            calls.append(L.Prepared(segs, tp, 0, 1e-6))
+        torch.cuda.synchronize()
+        ms = time_region(torch, lambda i: calls[i % nsets](), steps, warmup) / steps
+        pts.append((T, ms * 1e3))
+        del calls
+        torch.cuda.synchronize()
+        cms, _ = stream_copy_ms(torch, L, set_bytes, min_fp, steps, warmup, grids=(8192,))
+        cps.append((T, cms * 1e3))
+    out = {"widths": list(widths), "tp": tp, "bytes_per_token": algorithmic_bytes(1, widths, tp) -
+           4 * sum(widths)}
+    for key, data in (("fused", pts), ("copy", cps)):
+        t = np.array([p[0] for p in data], dtype=np.float64)
+        us = np.array([p[1] for p in data], dtype=np.float64)
+        slope, icpt = np.polyfit(t, us, 1)
+        out[key] = {"us": {int(a): round(b, 3) for a, b in data}, "intercept_us": round(icpt, 3),
+                    "slope_ns_per_token": round(slope * 1e3, 4),
+                    "streaming_gbs": round(out["bytes_per_token"] / (slope * 1e-6) / 1e9, 1)}
+    return out
+
+
 def time_graph(torch, fn, per_graph, replays):
     """Mean time (ms) per call when `per_graph` calls are replayed from one HIP graph."""
     fn(0)
@@ -351,14 +409,11 @@ def kernel_base_name(profiler_name: str) -> str:
 
 
 def summarize(outdir: str) -> None:
-    """Write the profile summaries of the headline kernel into profiles/ from
-    rocprofv3 CSV output in `outdir`:
-      trace/*_kernel_trace.csv and trace_bench.json -- kernel trace of the
-        default bench run and that run's JSON line;
-      pmc_fetch/, pmc_write/ -- FETCH_SIZE and WRITE_SIZE runs of
-        ``bench.py --no-extras --calibration-copy``.
-    Counters are scaled by what they read for the calibration copy (a plain
-    device copy of Q's input, known bytes)."""
+    """Write the kernel-trace summary of the headline kernel into profiles/
+    from rocprofv3 CSV output in `outdir`: trace/*_kernel_trace.csv and
+    trace_bench.json (the kernel trace of the default bench run and that run's
+    JSON line), next to bench.json (an untraced run of the same session), if
+    present. (The counter summaries come from --summarize-counters.)"""
     import csv
     import glob
     import statistics
@@ -422,40 +477,245 @@ def summarize(outdir: str) -> None:
     with open(os.path.join(ROOT, "profiles", f"trace_{tag}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
-    def counter(sub):
-        f = glob.glob(os.path.join(outdir, sub, "*_counter_collection.csv"))[0]
-        by = {}
-        for r in csv.DictReader(open(f)):
-            name = kernel_base_name(r["Kernel_Name"])
-            by.setdefault(name, []).append(float(r["Counter_Value"]))
-        return by
-    fetch, write = counter("pmc_fetch"), counter("pmc_write")
-    cal_f, cal_w = max(fetch["__amd_rocclr_copyBuffer"]), max(write["__amd_rocclr_copyBuffer"])
-    cal_bytes = bench["config"]["tokens"] * bench["config"]["q_local"] * (1 if "fp8" in kernel else 2)
-    sf, sw = cal_bytes / 1024 / cal_f, cal_bytes / 1024 / cal_w
-    kf, kw = statistics.mean(fetch[tname]), statistics.mean(write[tname])
-    hbm = int(round(kf * 1024 * sf + kw * 1024 * sw))
-    out = [f"kernel: {kernel} ({tname})", f"workload: {workload}", f"source_sha256: {sha}",
-           "commands (on the MI355X, from the repository root):",
-           "  rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o f -- python -u "
-           "bench.py --steps 20 --warmup 2 --no-cpu-baseline --no-extras --calibration-copy",
-           "  rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o w -- python -u "
-           "bench.py --steps 20 --warmup 2 --no-cpu-baseline --no-extras --calibration-copy",
-           "  python bench.py --summarize gpurun_out",
-           f"calibration copy (device copy of Q's input, {cal_bytes // 1024} KiB read and written):",
-           f"  FETCH_SIZE {cal_f:.1f} KiB -> scale {sf:.4f}",
-           f"  WRITE_SIZE {cal_w:.1f} KiB -> scale {sw:.4f}",
-           f"fused kernel, mean over {len(fetch[tname])} dispatches:",
-           f"  FETCH_SIZE {kf:.1f} KiB -> {int(round(kf * 1024 * sf))} bytes after scaling",
-           f"  WRITE_SIZE {kw:.1f} KiB -> {int(round(kw * 1024 * sw))} bytes after scaling",
-           f"algorithmic_bytes_per_launch: {algo}",
-           f"hbm_bytes_per_launch: {hbm}",
-           f"traffic_over_algorithmic: {hbm / algo:.4f}"]
-    with open(counters_path(kernel, workload), "w") as f:
-        f.write("\n".join(out) + "\n")
-    print("\n".join(out))
     print(f"trace: headline mean {mean_us:.3f} us over {len(headline)} dispatches; "
           f"bench kernel_us {bench['roofline']['kernel_us']}")
+
+
+# rocprofv3 --pmc passes over `bench.py --counter-pass` (each within the
+# per-block counter limits of one pass): HBM bytes, and the instruction-issue
+# counters behind the issue-rate comparison of fused and unfused kernels
+COUNTER_PASSES = (
+    ("pmc_fetch", "FETCH_SIZE"),
+    ("pmc_write", "WRITE_SIZE"),
+    ("pmc_issue", "SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_INSTS_VALU SQ_INSTS_SALU "
+                  "SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR"),
+    ("pmc_issue2", "GRBM_GUI_ACTIVE SQ_INSTS_SMEM SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY"),
+)
+COUNTER_STEPS = 20
+MARKER_KERNEL = "qkn_calib_empty_kernel"
+PROJ_SOURCES = [os.path.join(ROOT, "paper_2608_09160_amd", "csrc", "qkn_proj.hip")]
+
+
+def proj_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for path in PROJ_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def counter_pass(torch, L, workloads, min_fp: int) -> list:
+    """Each case: a few untimed launches, then a marker launch (the empty
+    calibration kernel), COUNTER_STEPS steps and another marker. Returns the case list
+    (tag, workload, algorithmic bytes per step, launch names of one step)."""
+    dev = "cuda:0"
+    cases = []
+
+    def run(tag, wl_name, nbytes, step, note="", launches=None):
+        for i in range(2):
+            step(i)
+        torch.cuda.synchronize()
+        names = []
+        L.qkn_calib_empty()  # start marker
+        for i in range(COUNTER_STEPS):
+            step(2 + i)
+            if i == 0:
+                names.append(L.qkn_last_launch()["kernel"] if launches is None else launches)
+        L.qkn_calib_empty()  # end marker
+        torch.cuda.synchronize()
+        cases.append({"tag": tag, "workload": wl_name, "bytes_per_step": nbytes, "note": note,
+                      "launch_names": names})
+        print(f"[counters] {tag} on {wl_name}", file=sys.stderr, flush=True)
+
+    # calibration: a plain device copy of known bytes
+    a = torch.empty(32 << 20, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    run("calibration_copy", "device copy of 32 MiB", 2 * a.numel(), lambda i: b.copy_(a),
+        launches="torch copy_")
+    del a, b
+    c4 = workloads.PREFILL_TP2
+    data = workloads.generate(c4)
+    case = Case(c4, 0, min_fp, torch, L, workloads, data=data)
+    run("fused", c4.name, case.bytes, case.launch)
+    two_bytes = case.bytes + sum(2 * s.x.numel() for s in case.sets[0])
+    run("two_step", c4.name, two_bytes, case.launch_two_step,
+        "Phase A per tensor, then Phases B+C per tensor: four launches per step",
+        launches="qkn_partial_sumsq Q, K; qkn_apply Q, K")
+    del case
+    g = GroupCase(c4, min_fp, torch, L, data)
+    run("group_wait", c4.name, g.bytes, g.launch, "every rank of the tp = 2 group in one launch")
+    del g
+    full = Case(c4.with_tp(1), 0, min_fp, torch, L, workloads, data=data, partials=False)
+    run("fused", c4.with_tp(1).name, full.bytes, full.launch, "tp = 1 full-vector baseline")
+    del full, data
+    c5 = workloads.LONG_PREFILL_TP4
+    long = Case(c5, 0, min_fp, torch, L, workloads)
+    run("fused", c5.name, long.bytes, long.launch)
+    del long
+    f8 = c4.with_dtype("fp8")
+    data8 = workloads.generate(f8)
+    p8 = Case(f8, 0, min_fp, torch, L, workloads, data=data8)
+    run("fused", f8.name, p8.bytes, p8.launch)
+    del p8
+    g8 = GroupCase(f8, min_fp, torch, L, data8)
+    run("group_wait", f8.name, g8.bytes, g8.launch, "every rank of the tp = 2 group in one launch")
+    del g8, data8
+    # the decode-sized projection (warm: the same buffers every call, as in its timing)
+    dwl = workloads.DECODE_TP4
+    pdata = workloads.projection_inputs(dwl)
+
+    def bf16(arr):
+        arr = np.ascontiguousarray(arr, dtype=np.uint16)
+        return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).to(dev)
+    x = bf16(pdata["x"])
+    wq = bf16(pdata["wq"][workloads.shard_cols(dwl.q_full, dwl.tp, 1)])
+    wk = bf16(pdata["wk"][workloads.shard_cols(dwl.k_full, dwl.tp, 1)])
+    prep = L.PreparedProj(x, [L.ProjSeg(w=wq), L.ProjSeg(w=wk)])
+    cols, hidden = wq.shape[0] + wk.shape[0], x.shape[1]
+    run("proj", dwl.name, 2 * (cols * hidden + dwl.T * hidden + dwl.T * cols), lambda i: prep(),
+        "split-k projection and its reduction: two launches per call; weights warm")
+    torch.cuda.synchronize()
+    return cases
+
+
+def _counter_rows(path: str):
+    """{(dispatch id, kernel base name): {counter: value}} from one --pmc CSV, in dispatch order."""
+    import csv
+    import glob
+    f = glob.glob(os.path.join(path, "*_counter_collection.csv"))[0]
+    by = {}
+    for r in csv.DictReader(open(f)):
+        key = (int(r["Dispatch_Id"]), kernel_base_name(r["Kernel_Name"]))
+        by.setdefault(key, {})[r["Counter_Name"]] = by.get(key, {}).get(r["Counter_Name"], 0.0) + \
+            float(r["Counter_Value"])
+    return [(k[1], v) for k, v in sorted(by.items())]
+
+
+def _split_cases(rows, ncases):
+    """The dispatches between each case's start and end marker launches."""
+    segs, cur = [], None
+    for name, vals in rows:
+        if name.startswith(MARKER_KERNEL):
+            if cur is None:
+                cur = []
+            else:
+                segs.append(cur)
+                cur = None
+        elif cur is not None:
+            cur.append((name, vals))
+    if len(segs) != ncases:
+        raise ValueError(f"{len(segs)} marker segments, {ncases} cases")
+    return segs
+
+
+def _per_kernel_means(seg, counter):
+    """Mean per dispatch of `counter` for each kernel of a case, in first-seen order."""
+    order, vals = [], {}
+    for name, v in seg:
+        if counter in v:
+            if name not in vals:
+                order.append(name)
+                vals[name] = []
+            vals[name].append(v[counter])
+    return [(n, float(np.mean(vals[n])), len(vals[n])) for n in order]
+
+
+def summarize_counters(outdir: str) -> None:
+    """profiles/counters_<kernel>_<workload>.txt for every case of the counter
+    pass (HBM bytes per step from FETCH_SIZE and WRITE_SIZE, each scaled by
+    what it reads for a device copy of known size) and
+    profiles/issue_rate_<workload>.md (instruction-issue counters of the fused,
+    two-launch and group-wait kernels on the prefill shard)."""
+    cases = json.loads(open(os.path.join(outdir, "counter_pass.json")).read().strip().splitlines()[-1])
+    segs = {tag: _split_cases(_counter_rows(os.path.join(outdir, tag)), len(cases))
+            for tag, _ in COUNTER_PASSES}
+    cal = 0
+    cal_f = sum(m for _, m, _ in _per_kernel_means(segs["pmc_fetch"][cal], "FETCH_SIZE"))
+    cal_w = sum(m for _, m, _ in _per_kernel_means(segs["pmc_write"][cal], "WRITE_SIZE"))
+    half = cases[cal]["bytes_per_step"] // 2
+    sf, sw = half / 1024 / cal_f, half / 1024 / cal_w
+    sha, psha = source_sha256(), proj_sha256()
+    cmds = ["python -u bench.py --counter-pass > gpurun_out/counters/counter_pass.json"] + [
+        f"rocprofv3 --pmc {ctrs} --output-format csv -d gpurun_out/counters/{tag} -o c -- "
+        f"python -u bench.py --counter-pass" for tag, ctrs in COUNTER_PASSES] + [
+        "python bench.py --summarize-counters gpurun_out/counters"]
+    written = []
+    for i, c in enumerate(cases):
+        if i == cal:
+            continue
+        fetch = _per_kernel_means(segs["pmc_fetch"][i], "FETCH_SIZE")
+        write = dict((n, (m, k)) for n, m, k in _per_kernel_means(segs["pmc_write"][i], "WRITE_SIZE"))
+        kernels = [n for n, _, _ in fetch]
+        per_step = COUNTER_STEPS
+        lines = []
+        hbm = 0.0
+        for n, mf, k in fetch:
+            mw, _ = write[n]
+            reps = k / per_step  # dispatches of this kernel per step
+            bf, bw = mf * 1024 * sf * reps, mw * 1024 * sw * reps
+            hbm += bf + bw
+            lines.append(f"  {n}: {k} dispatches ({reps:g} per step); FETCH_SIZE {mf:.1f} KiB, "
+                         f"WRITE_SIZE {mw:.1f} KiB per dispatch -> {int(round(bf))} + "
+                         f"{int(round(bw))} bytes per step after scaling")
+        proj = c["tag"] == "proj"
+        fname = (f"counters_two_step_{c['workload']}.txt" if c["tag"] == "two_step"
+                 else os.path.basename(counters_path(c["launch_names"][0], c["workload"])))
+        out = [f"launches of one step: {', '.join(c['launch_names'])}" +
+               (f" ({c['note']})" if c.get("note") else ""),
+               f"profiler names: {', '.join(kernels)}",
+               f"workload: {c['workload']}",
+               (f"source_sha256 (qkn_proj.hip): {psha}" if proj else f"source_sha256: {sha}"),
+               "commands (on the MI355X, from the repository root):"] + [f"  {x}" for x in cmds] + [
+               f"calibration copy ({half // 1024} KiB read and written): FETCH_SIZE {cal_f:.1f} KiB "
+               f"-> scale {sf:.4f}; WRITE_SIZE {cal_w:.1f} KiB -> scale {sw:.4f}",
+               f"per kernel, mean over the {per_step} steps between the marker launches:"] + lines + [
+               f"algorithmic_bytes_per_launch: {c['bytes_per_step']}",
+               f"hbm_bytes_per_launch: {int(round(hbm))}",
+               f"traffic_over_algorithmic: {hbm / c['bytes_per_step']:.4f}"]
+        with open(os.path.join(ROOT, "profiles", fname), "w") as f:
+            f.write("\n".join(out) + "\n")
+        written.append((fname, hbm / c["bytes_per_step"]))
+    # issue rate on the prefill shard: fused, two-launch, group wait
+    keys = ("SQ_WAVES", "SQ_BUSY_CYCLES", "SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_INSTS_VALU",
+            "SQ_INSTS_SALU", "SQ_INSTS_VMEM_RD", "SQ_INSTS_VMEM_WR")
+    keys2 = ("GRBM_GUI_ACTIVE", "SQ_INSTS_SMEM", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY")
+    c4 = cases[1]["workload"]
+    rows = ["| case | kernels per step | waves | instructions (VALU+SALU+VMEM+SMEM) | "
+            "SQ_BUSY_CYCLES | GRBM_GUI_ACTIVE | instructions per busy cycle | "
+            "SQ_WAIT_ANY / SQ_WAVE_CYCLES | SQ_ACTIVE_INST_ANY / SQ_WAVE_CYCLES |",
+            "|---|---|---|---|---|---|---|---|---|"]
+    rate = {}
+    for i, c in enumerate(cases):
+        if c["workload"] != c4 or c["tag"] not in ("fused", "two_step", "group_wait"):
+            continue
+        tot = {}
+        for k in keys:
+            tot[k] = sum(m * (n_ / COUNTER_STEPS) for _, m, n_ in _per_kernel_means(segs["pmc_issue"][i], k))
+        for k in keys2:
+            tot[k] = sum(m * (n_ / COUNTER_STEPS) for _, m, n_ in _per_kernel_means(segs["pmc_issue2"][i], k))
+        inst = tot["SQ_INSTS_VALU"] + tot["SQ_INSTS_SALU"] + tot["SQ_INSTS_VMEM_RD"] + \
+            tot["SQ_INSTS_VMEM_WR"] + tot["SQ_INSTS_SMEM"]
+        rate[c["tag"]] = inst / tot["SQ_BUSY_CYCLES"]
+        rows.append(f"| {c['tag']} | {', '.join(c['launch_names'])} | {tot['SQ_WAVES']:.0f} | {inst:.3e} | "
+                    f"{tot['SQ_BUSY_CYCLES']:.3e} | {tot['GRBM_GUI_ACTIVE']:.3e} | {rate[c['tag']]:.2f} | "
+                    f"{tot['SQ_WAIT_ANY'] / tot['SQ_WAVE_CYCLES']:.3f} | "
+                    f"{tot['SQ_ACTIVE_INST_ANY'] / tot['SQ_WAVE_CYCLES']:.3f} |")
+    md = [f"# Instruction issue on the prefill shard ({c4})", "",
+          f"Kernel source sha256 {sha}. Commands (MI355X, repository root):", ""] + \
+         [f"    {x}" for x in cmds] + ["",
+          "Counters summed over the kernels of one step (means per dispatch times dispatches per "
+          "step). instructions = SQ_INSTS_VALU + SQ_INSTS_SALU + SQ_INSTS_VMEM_RD + "
+          "SQ_INSTS_VMEM_WR + SQ_INSTS_SMEM; SQ_BUSY_CYCLES counts the cycles the sequencers are "
+          "busy, so instructions per busy cycle is the issue-rate analogue of a GPU-wide "
+          "instruction rate.", ""] + rows
+    if "fused" in rate and "two_step" in rate:
+        md += ["", f"Issue rate, fused over two-launch: {rate['fused'] / rate['two_step']:.2f}x."]
+    with open(os.path.join(ROOT, "profiles", f"issue_rate_{c4}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    for fname, ratio in written:
+        print(f"{fname}: traffic / algorithmic {ratio:.4f}")
+    print("\n".join(md[-len(rows) - 2:]))
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
@@ -539,6 +799,7 @@ def summarize_proj(outdir: str) -> None:
                 continue
             rows[key][r["Counter_Name"]].append(float(r["Counter_Value"]))
     lines = ["Q/K projection, 8192 tokens x hidden 4096 -> 2048 + 512 columns (bf16, fp32 accumulation)",
+             f"source_sha256 (qkn_proj.hip): {proj_sha256()}",
              "commands (on the MI355X, from the repository root):"]
     lines += ["  " + c for c in cmds]
     lines += ["  python bench.py --summarize-proj gpurun_out",
@@ -577,7 +838,20 @@ def cpu_baseline(wl, rank, data, seconds):
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} full passes over the {T}-token workload (rank {rank}), "
                       f"{round(el, 2)} s of fp64 numpy on one thread",
-            "host_cpus_visible": ncpu, "cpu_model": platform.processor() or platform.machine()}
+            "host_cpus_visible": ncpu, "cpu_model": cpu_model(),
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), else the machine type."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def main():
@@ -588,13 +862,15 @@ def main():
     if args.summarize_proj:
         summarize_proj(args.summarize_proj)
         return 0
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU's share of the sharded QK-Norm; the peer ranks "
               "are simulated in device memory. Runs on more than one GPU are not supported: "
               "use --gpus 1.", file=sys.stderr)
         return 2
-    os.environ.setdefault("OMP_NUM_THREADS", "1")
     import torch
     import workloads
     from paper_2608_09160_amd import _lib as L
@@ -607,6 +883,9 @@ def main():
     if args.proj_only:
         out = {"proj_partial_prefill": proj_extra(torch, L, workloads, wl, args.rank, steps=10)}
         print(json.dumps(out), flush=True)
+        return 0
+    if args.counter_pass:
+        print(json.dumps(counter_pass(torch, L, workloads, args.min_footprint_mb << 20)), flush=True)
         return 0
     data = workloads.generate(wl)
     min_fp = args.min_footprint_mb << 20
@@ -649,6 +928,9 @@ def main():
             "bytes": copy_bytes, "us_per_step": round(cms * 1e3, 3), "blocks": cblocks,
             "gbs": round(copy_bytes / (cms * 1e-3) / 1e9, 1),
             "fused_kernel_frac_of_copy": round(cms / ms_per_step, 4)}
+        # the fixed cost per launch and the streaming rate: launch time against
+        # the token count at the prefill shard's widths, kernel and copy
+        extras["time_vs_tokens"] = token_fit(torch, L, min_fp, args.steps, args.warmup)
         # the launch floor: an empty kernel replayed from a HIP graph
         us = time_graph(torch, lambda i: L.qkn_calib_empty(), 200, 10) * 1e3
         extras["empty_kernel_graph"] = {"us_per_launch_graph": round(us, 3)}

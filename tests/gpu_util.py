@@ -133,15 +133,15 @@ def for_each_oracle_block(wl: workloads.Workload, data, fn, rows=None,
             pass
 
 
-def check_y(got_bits: np.ndarray, ref_y: np.ndarray, fmt: str, what: str) -> None:
+def check_y(got_bits: np.ndarray, ref_y: np.ndarray, fmt: str, what: str) -> float:
     """Outputs against the oracle: bf16 within the relative tolerance, FP8 as
-    the round-to-nearest-even code of a value within the noise band."""
+    the round-to-nearest-even code of a value within the noise band. Returns
+    the largest relative error (bf16) or error in half FP8 steps (FP8)."""
     from oracle import compare
     from oracle import qknorm as Q
     if fmt == "fp8":
-        compare.check_fp8(Q.decode_e4m3(got_bits), ref_y, what)
-    else:
-        compare.check_close(Q.decode_bf16(got_bits), ref_y, compare.OUTPUT_RTOL, what)
+        return compare.check_fp8(Q.decode_e4m3(got_bits), ref_y, what)
+    return compare.check_close(Q.decode_bf16(got_bits), ref_y, compare.OUTPUT_RTOL, what)
 
 
 def check_rank_every_token(wl: workloads.Workload, data, rank: int, out, what: str,
@@ -158,21 +158,28 @@ def check_ranks_every_token(wl: workloads.Workload, data, outs, what: str, rows=
     """check_rank_every_token for several ranks' results ({rank: out}) with
     one pass of the oracle."""
     from oracle import compare
+    worst = {"y": [0.0], "statistic": [0.0], "inv": [0.0]}
 
     def fn(sel, ref):
         for rank, out in outs.items():
             for t, d_full in (("q", wl.q_full), ("k", wl.k_full)):
                 cols = workloads.shard_cols(d_full, wl.tp, rank)
                 o = out[t]
-                check_y(o["y"][sel], ref[t]["y"][:, cols], wl.dtype, f"{what} {t} y r{rank}")
+                worst["y"].append(check_y(o["y"][sel], ref[t]["y"][:, cols], wl.dtype,
+                                          f"{what} {t} y r{rank}"))
                 if o.get("partials") is not None:
-                    compare.check_close(o["partials"][rank][sel], ref[t]["partials"][rank],
-                                        compare.PARTIAL_RTOL, f"{what} {t} own statistic r{rank}")
+                    worst["statistic"].append(compare.check_close(
+                        o["partials"][rank][sel], ref[t]["partials"][rank],
+                        compare.PARTIAL_RTOL, f"{what} {t} own statistic r{rank}"))
                 if o.get("inv") is not None:
-                    compare.check_close(o["inv"][sel], ref[t]["inv"], 1e-5,
-                                        f"{what} {t} inv r{rank}")
+                    worst["inv"].append(compare.check_close(o["inv"][sel], ref[t]["inv"], 1e-5,
+                                                            f"{what} {t} inv r{rank}"))
 
     for_each_oracle_block(wl, data, fn, rows)
+    unit = "half FP8 steps" if wl.dtype == "fp8" else "relative"
+    print(f"[errors] {what}: ranks {sorted(outs)}, max y error {max(worst['y']):.3e} ({unit}), "
+          f"max statistic rel error {max(worst['statistic']):.3e}, max factor rel error "
+          f"{max(worst['inv']):.3e}", flush=True)
 
 
 def slot_values(slots: np.ndarray, epoch: int) -> np.ndarray:

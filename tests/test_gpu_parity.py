@@ -30,14 +30,17 @@ SMALL = [workloads.TINY_FULL, workloads.DECODE_TP4, workloads.DECODE_TP8,
 
 def _check_rank(wl, data, rank, out):
     ref = Q.qknorm_layerwise(data["xq"], data["xk"], data["gq"], data["gk"], wl.tp, rank, wl.eps)
+    ey, ep = [], []
     for t in "qk":
         r = ref[t]
         got = out[t]
-        compare.check_close(Q.decode_bf16(got["y"]), r["y"], compare.OUTPUT_RTOL,
-                            f"{wl.name} rank {rank} {t} y")
-        compare.check_close(got["partials"][rank], r["partials"][rank], compare.PARTIAL_RTOL,
-                            f"{wl.name} rank {rank} {t} partial")
+        ey.append(compare.check_close(Q.decode_bf16(got["y"]), r["y"], compare.OUTPUT_RTOL,
+                                      f"{wl.name} rank {rank} {t} y"))
+        ep.append(compare.check_close(got["partials"][rank], r["partials"][rank],
+                                      compare.PARTIAL_RTOL, f"{wl.name} rank {rank} {t} partial"))
         compare.check_close(got["inv"], r["inv"], 1e-5, f"{wl.name} rank {rank} {t} inv")
+    print(f"[errors] {wl.name} rank {rank}: max y rel error {max(ey):.3e}, max statistic rel "
+          f"error {max(ep):.3e}", flush=True)
 
 
 @pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
