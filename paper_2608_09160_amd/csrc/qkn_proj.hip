@@ -469,15 +469,26 @@ __device__ __forceinline__ void load16_to_lds(Rsrc r, LdsByte* dst, uint32_t vof
 // [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8])
 constexpr int vmcnt_imm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
 
+// Wait until at most n vector-memory requests of this wavefront are in flight
+// (n is wavefront-uniform; the instruction takes the count as an immediate,
+// so every count a caller can pass has its own case; larger counts wait for
+// all).
 __device__ __forceinline__ void vm_wait(int n) {
+#define QKN_VM_CASE(k) \
+  case k:              \
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(k)); \
+    break;
   switch (n) {
-    case 4: __builtin_amdgcn_s_waitcnt(vmcnt_imm(4)); break;
-    case 8: __builtin_amdgcn_s_waitcnt(vmcnt_imm(8)); break;
-    case 12: __builtin_amdgcn_s_waitcnt(vmcnt_imm(12)); break;
-    case 16: __builtin_amdgcn_s_waitcnt(vmcnt_imm(16)); break;
-    case 24: __builtin_amdgcn_s_waitcnt(vmcnt_imm(24)); break;
+    QKN_VM_CASE(1) QKN_VM_CASE(2) QKN_VM_CASE(3) QKN_VM_CASE(4) QKN_VM_CASE(5) QKN_VM_CASE(6)
+    QKN_VM_CASE(7) QKN_VM_CASE(8) QKN_VM_CASE(9) QKN_VM_CASE(10) QKN_VM_CASE(11) QKN_VM_CASE(12)
+    QKN_VM_CASE(13) QKN_VM_CASE(14) QKN_VM_CASE(15) QKN_VM_CASE(16) QKN_VM_CASE(17)
+    QKN_VM_CASE(18) QKN_VM_CASE(19) QKN_VM_CASE(20) QKN_VM_CASE(21) QKN_VM_CASE(22)
+    QKN_VM_CASE(23) QKN_VM_CASE(24) QKN_VM_CASE(25) QKN_VM_CASE(26) QKN_VM_CASE(27)
+    QKN_VM_CASE(28) QKN_VM_CASE(29) QKN_VM_CASE(30) QKN_VM_CASE(31) QKN_VM_CASE(32)
+    QKN_VM_CASE(36) QKN_VM_CASE(40) QKN_VM_CASE(48) QKN_VM_CASE(56)
     default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;  // 0, and any count not listed
   }
+#undef QKN_VM_CASE
 }
 
 // Main loop of one direct-to-LDS tile: BM = 64 WMB rows from m0 (rows_a of
@@ -544,9 +555,13 @@ __device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDe
       for (int r = 0; r < A::kR; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = (k_hi - k_lo + BK - 1) / BK;
+  // A k-range of at most S stages is requested whole before the first
+  // MFMA (every stage has its own ring slot); a longer one keeps S - 1
+  // stages in flight and requests the next into the slot just consumed.
+  const int pre = nk <= S ? nk : S - 1;
 #pragma unroll
-  for (int st = 0; st < S - 1; ++st)
-    if (st < nk) QKN_ISSUE_STAGE(st, k_lo + st * BK);
+  for (int st = 0; st < S; ++st)
+    if (st < pre) QKN_ISSUE_STAGE(st, k_lo + st * BK);
 
   // MI = 32: lane l supplies row (l mod 32) of a 32-row block and k-values
   // 8 (l / 32) .. 8 (l / 32) + 7 of a 16-deep k-block; MI = 16: row (l mod 16)
@@ -556,15 +571,15 @@ __device__ __forceinline__ void dl_mainloop(const ProjParams& p, const ProjSegDe
   constexpr int kKBlock = 512 / MI;  // k per MFMA
   constexpr int kPerStage = C::kLoadsA + C::kLoadsB;  // load instructions per wave per stage
   for (int kt = 0; kt < nk; ++kt) {
-    // stages kt + 1 .. kt + S - 2 may stay in flight
-    const int later = (nk - 1 - kt < S - 2) ? nk - 1 - kt : S - 2;
+    // the stages requested after stage kt may stay in flight
+    const int later = (nk - 1 - kt < pre - 1) ? nk - 1 - kt : pre - 1;
     vm_wait(later * kPerStage);
     // A plain barrier, not __syncthreads(): its fence would wait for every
     // load in flight, the later stages' too. Each wavefront has waited for its
     // own part of stage kt (the DMA count drops once the data is in LDS), and
     // its reads of stage kt - 1 were consumed by MFMAs before it got here.
     __builtin_amdgcn_s_barrier();
-    if (kt + S - 1 < nk) QKN_ISSUE_STAGE(kt + S - 1, k_lo + (kt + S - 1) * BK);
+    if (pre < nk && kt + S - 1 < nk) QKN_ISSUE_STAGE(kt + S - 1, k_lo + (kt + S - 1) * BK);
     const unsigned char* a = lds + (kt % S) * C::kStageBytes;
     const unsigned char* b = a + C::kTileBytesA;
 #pragma unroll
@@ -668,11 +683,19 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams
   using A = AccOf<MI, WMB>;
   typename A::T acc;
   dl_mainloop<MI, WMB, BK, S>(p, s, lds, t.m0, t.n0, t.rows_a, t.rows_b, k_lo, k_hi, acc);
-  // fp32 sums of this k-slice: lanes 0..MI-1 of a row are MI adjacent columns
-  const int lane = static_cast<int>(threadIdx.x) & 63;
-  const int wave = static_cast<int>(threadIdx.x) >> 6;
+  // fp32 sums of this k-slice, through LDS: the accumulators (lanes 0..MI-1
+  // of a row hold MI adjacent columns) go to an fp32 tile in LDS, which is
+  // then written out row by row in 16-byte vectors (4-byte stores straight
+  // from the accumulators scatter every wave instruction over 4 rows).
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  float* part = p.part + static_cast<int64_t>(ks) * p.T * p.ncols;
+  constexpr int kBM = C::BM, kBN = C::BN;
+  constexpr int kRow = kBN + 4;  // padded: the four 16-lane row groups of a write use other banks
+  static_assert(kBM * kRow * 4 <= C::kLdsBytes, "the fp32 tile fits in the stage buffers");
+  float* tile = reinterpret_cast<float*>(lds);
+  __syncthreads();  // every wavefront is done reading the stages
 #pragma unroll
   for (int i = 0; i < A::kM; ++i)
 #pragma unroll
@@ -683,10 +706,21 @@ __global__ __launch_bounds__(kThreads) void qkn_proj_gemm_split(const ProjParams
         const int row = (MI == 32)
             ? wm * 32 * WMB + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)
             : wm * 32 * WMB + i * 16 + 4 * (lane >> 4) + r;
-        if (row < t.rows_a && col < t.rows_b)
-          part[(t.m0 + row) * p.ncols + s.col0 + t.n0 + col] = acc[i][j][r];
+        tile[row * kRow + col] = acc[i][j][r];
       }
     }
+  __syncthreads();
+  // a row's valid columns are a multiple of 8 (d_local is), and its first
+  // column's offset in the slice array is a multiple of 8 floats, so every
+  // vector is whole and 16-byte aligned
+  float* part = p.part + static_cast<int64_t>(ks) * p.T * p.ncols + t.m0 * p.ncols + s.col0 + t.n0;
+  constexpr int kVecs = kBN / 4;
+  for (int q = tid; q < kBM * kVecs; q += kThreads) {
+    const int row = q / kVecs, c4 = (q % kVecs) * 4;
+    if (row < t.rows_a && c4 < t.rows_b)
+      *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(row) * p.ncols + c4) =
+          *reinterpret_cast<const f32x4*>(tile + row * kRow + c4);
+  }
 }
 
 // Split-k reduction, one workgroup per token and segment (the segments'
