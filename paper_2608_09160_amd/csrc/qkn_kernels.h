@@ -271,7 +271,9 @@ constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
 #define QKN_LOAD_CPOL 2  // non-temporal
 #endif
 #ifndef QKN_STORE_CPOL
-#define QKN_STORE_CPOL 18  // non-temporal, system scope (sc1 nt): measured best for y
+// non-temporal (nt): the prefill shapes run as with sc1 nt (within 1 %), and
+// decode-sized launches, whose stores end the launch, 5 % faster
+#define QKN_STORE_CPOL 2
 #endif
 constexpr int kLoadCpol = QKN_LOAD_CPOL;    // cache policy of the streamed x
 constexpr int kStoreCpol = QKN_STORE_CPOL;  // cache policy of the streamed y
