@@ -1,8 +1,11 @@
 """GPU: the prepared entry points captured in a HIP graph (decode serving
 loops replay them). Every replay must equal the eager result bit for bit; the
 replays are separated by eager work that overwrites the outputs, so a replay
-that wrote nothing, or wrote stale values, is caught. The library allocates
-nothing and records no memset, so its launches are capturable as they are.
+that wrote nothing, or wrote stale values, is caught; the eager result and
+every replay are also checked against the fp64 oracle (the norm on every
+token and rank it computes, the projection within its rounding bound). The
+library allocates nothing and records no memset, so its launches are
+capturable as they are.
 
 The Phase B wait entry points take the round's epoch as a launch argument,
 which a captured launch keeps; their graph clears the slot arrays with a
@@ -18,7 +21,12 @@ import torch
 import workloads
 from paper_2608_09160_amd import _lib as L
 
-from gpu_util import DEV, inputs, peer_partials, to_dev_act, to_dev_bf16, to_dev_f32
+from oracle import compare
+from oracle import projection as P_oracle
+from oracle import qknorm as Q
+
+from gpu_util import (DEV, bits_of, check_group_every_token, check_rank_every_token, inputs,
+                      peer_partials, to_dev_act, to_dev_bf16, to_dev_f32)
 
 pytestmark = pytest.mark.gpu
 
@@ -54,9 +62,13 @@ def _graph_of(fn):
     return g
 
 
-def _check_replays(fn, outs, clobber):
+def _check_replays(fn, outs, clobber, oracle_check=None):
+    """Eager result, then REPLAYS replays each equal to it bit for bit;
+    oracle_check(outputs) runs on the eager result and on every replay."""
     fn()
     ref = _outputs(outs)
+    if oracle_check is not None:
+        oracle_check(ref)
     g = _graph_of(fn)
     for r in range(REPLAYS):
         clobber(r)                       # eager work between replays
@@ -65,6 +77,8 @@ def _check_replays(fn, outs, clobber):
         got = _outputs(outs)
         for a, b in zip(ref, got):
             assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"replay {r}"
+        if oracle_check is not None:
+            oracle_check(got)
 
 
 @pytest.mark.parametrize("wl,rank", [(workloads.DECODE_TP4, 1), (workloads.DECODE_TP8, 7),
@@ -80,7 +94,12 @@ def test_fused_shard_graph_replays(wl, rank):
             s.y.view(torch.uint8).fill_(0x7F)
             s.inv_rms.fill_(float(r))
             s.partials[rank].fill_(-1.0)
-    _check_replays(prep, outs, clobber)
+
+    def oracle_check(got):
+        out = {t: {"y": bits_of(got[3 * i]), "inv": got[3 * i + 1].cpu().numpy(),
+                   "partials": got[3 * i + 2].cpu().numpy()} for i, t in enumerate("qk")}
+        check_rank_every_token(wl, inputs(wl), rank, out, f"{wl.name} graph")
+    _check_replays(prep, outs, clobber, oracle_check)
 
 
 @pytest.mark.parametrize("T,hidden,dq,dk", [(64, 4096, 1024, 256), (1300, 1096, 264, 136)])
@@ -100,7 +119,19 @@ def test_projection_graph_replays(T, hidden, dq, dk):
             s.y.view(torch.uint8).fill_(0x55)
             s.partials.fill_(float(r))
         prep.workspace.fill_(0xFF)
-    _check_replays(prep, outs, clobber)
+    x_bits = bits_of(x)
+    w_bits = [bits_of(w) for w in ws]
+    q_exact = [P_oracle.project(x_bits, wb) for wb in w_bits]
+    dot_abs = [P_oracle.dot_abs(x_bits, wb) for wb in w_bits]
+    stat = [P_oracle.stored_partials(x_bits, wb) for wb in w_bits]
+
+    def oracle_check(got):
+        for i in range(2):
+            yv = Q.decode_bf16(bits_of(got[2 * i]))
+            compare.check_projection(yv, q_exact[i], dot_abs[i], hidden, f"graph proj seg{i} y")
+            err = np.abs(got[2 * i + 1].cpu().numpy().astype(np.float64) - stat[i])
+            assert np.all(err <= compare.projection_partial_bound(q_exact[i], dot_abs[i], hidden))
+    _check_replays(prep, outs, clobber, oracle_check)
 
 
 @pytest.mark.parametrize("wl", [workloads.DECODE_TP4, workloads.DECODE_TP8.with_dtype("fp8")],
@@ -134,7 +165,13 @@ def test_group_wait_graph_with_slots_cleared_in_the_graph(wl):
             s.inv_rms.fill_(float(r))
         for s in slots:
             s.fill_(stale)
-    _check_replays(step, [s.y for s in segs] + [s.inv_rms for s in segs], clobber)
+
+    def oracle_check(got):
+        check_group_every_token(wl, data, {"q": bits_of(got[0]), "k": bits_of(got[1])},
+                                {"q": got[2].cpu().numpy(), "k": got[3].cpu().numpy()},
+                                {t: sl.cpu().numpy() for t, sl in zip("qk", slots)}, epoch,
+                                f"{wl.name} graph")
+    _check_replays(step, [s.y for s in segs] + [s.inv_rms for s in segs], clobber, oracle_check)
     assert int(status.item()) == 0
 
 
@@ -165,4 +202,13 @@ def test_prepared_apply_equals_apply_and_replays(wl, rank):
     def clobber(r):
         prep.y.view(torch.uint8).fill_(0x7F)
         prep.inv_rms.fill_(float(r))
-    _check_replays(prep, [prep.y, prep.inv_rms], clobber)
+    ref_o = Q.qknorm_shard(data["xq"], data["gq"], wl.tp, rank, wl.eps, fmt=wl.dtype)
+
+    def oracle_check(got):
+        yb = bits_of(got[0])
+        if wl.dtype == "fp8":
+            compare.check_fp8(Q.decode_e4m3(yb), ref_o["y"], "graph apply y")
+        else:
+            compare.check_close(Q.decode_bf16(yb), ref_o["y"], compare.OUTPUT_RTOL, "graph apply y")
+        compare.check_close(got[1].cpu().numpy(), ref_o["inv"], 1e-5, "graph apply inv")
+    _check_replays(prep, [prep.y, prep.inv_rms], clobber, oracle_check)
