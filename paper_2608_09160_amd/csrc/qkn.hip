@@ -409,7 +409,7 @@ int launch(const HSeg* segs, int nseg, int tp, int rank, int64_t T, float eps, i
   // Persistent grid: enough wavefronts per CU to keep about fi.inflight_bytes
   // of rows requested per CU, at least kMinWavesPerCu, at most what fits.
   int64_t waves_per_cu = static_cast<int64_t>(bpc) * wpb;
-  if ((fast || wide) && mode != kFusedWait) {  // a waiting launch keeps every resident slot
+  if (fast || wide) {  // waiting launches too: fewer waves only loosen the co-residency bound below
     int64_t token_bytes = 0;
     for (int i = 0; i < nseg; ++i) token_bytes += fi.esz * static_cast<int64_t>(kp.seg[i].d);
     int64_t want = (fi.inflight_bytes + token_bytes - 1) / token_bytes;
