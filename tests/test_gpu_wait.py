@@ -226,3 +226,32 @@ def test_epochs_reuse_slots_without_reset():
     torch.cuda.synchronize()
     assert int(status.item()) == 1
     assert torch.isnan(segs[0].y.float()).all()
+
+
+def _random_group(rng, i):
+    fmt = "fp8" if rng.random() < 0.4 else "bf16"
+    per = 16 if fmt == "fp8" else 8           # elements per 16-byte chunk: the register path's unit
+    tp = int(rng.choice([2, 3, 4, 5, 8]))
+    q_local = int(rng.integers(1, 4096 // per + 1)) * per
+    k_local = int(rng.integers(1, 1024 // per + 1)) * per
+    T = int(np.exp(rng.uniform(0, np.log(3000))))
+    dist = str(rng.choice(["normal", "normal_lognormal", "normal_outliers", "student_t"]))
+    wl = workloads.Workload(f"random{i}_T{T}_q{q_local * tp}_k{k_local * tp}_tp{tp}", T,
+                            q_local * tp, k_local * tp, tp, dist, 500 + i, sigma=0.7)
+    return wl.with_dtype("fp8") if fmt == "fp8" else wl, int(rng.integers(0, 5))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_groups_against_oracle(seed):
+    """Seeded random whole-group waits: token counts 1..3000, tp 2..8, slice
+    widths across the register path of both formats, all five schedules;
+    every token and rank against the oracle (through _run_group_and_check)."""
+    rng = np.random.default_rng(7000 + seed)
+    for i in range(3):
+        wl, sched = _random_group(rng, 10 * seed + i)
+        print(f"[wait] random group {wl.name} schedule {sched}", flush=True)
+        L.qkn_set_option("wait_schedule", sched)
+        try:
+            _run_group_and_check(wl)
+        finally:
+            L.qkn_set_option("wait_schedule", 4)
