@@ -115,7 +115,8 @@ int qkn_proj_partial(const uint16_t* x, int64_t ldx, int64_t T, int64_t hidden,
  * workspace taken from a fixed per-device array of QKN_PROJ_SCRATCH_BYTES
  * instead of an argument. It calls no allocator (no hipMalloc, no hipFree);
  * its first call on a device looks the array's address up once (a runtime
- * query, no allocation). Every call on one GPU shares that GPU's array, which
+ * query, no allocation; code that captures a HIP graph makes that first call
+ * before capturing). Every call on one GPU shares that GPU's array, which
  * keeps the last call's contents (no call needs it cleared: every workspace
  * byte a call's kernels read was written earlier by the same call's kernels,
  * in stream order); calls that overlap in time on

@@ -96,3 +96,63 @@ def test_noalloc_rejects_a_workspace_beyond_its_size():
     with pytest.raises(L.QknError) as e:
         L.qkn_proj_partial_noalloc(x, segs)
     assert e.value.status == L.QKN_ENOTSUP
+
+
+def _graph_of(fn):
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    return g
+
+
+@pytest.mark.parametrize("shape,other", [((64, 4096, 1024, 256), (300, 1024, 512, 128)),
+                                         ((300, 1024, 512, 128), (64, 4096, 1024, 256))],
+                         ids=["split_k", "chunk_statistics"])
+def test_noalloc_graph_replays(shape, other):
+    """The caller this entry point is for: a captured graph replayed while eager
+    calls of another shape reuse the same fixed workspace in between. Every
+    replay equals the eager result bit for bit and stays within the oracle's
+    bounds. One eager call precedes the capture (it looks the array's address up)."""
+    T, hidden, dq, dk = shape
+    print(f"[noalloc graph] T={T} hidden={hidden} q={dq} k={dk}", flush=True)
+    x_bits, w_bits = _inputs(T, hidden, dq, dk, 300)
+    x = to_dev_bf16(x_bits)
+    segs = [L.ProjSeg(w=to_dev_bf16(w), y=torch.empty((T, w.shape[0]), dtype=torch.bfloat16,
+                                                     device=DEV),
+                      partials=torch.empty(T, dtype=torch.float32, device=DEV)) for w in w_bits]
+    oT, oh, oq, ok = other
+    ox_bits, ow_bits = _inputs(oT, oh, oq, ok, 400)
+    ox = to_dev_bf16(ox_bits)
+    osegs = [L.ProjSeg(w=to_dev_bf16(w), y=torch.empty((oT, w.shape[0]), dtype=torch.bfloat16,
+                                                       device=DEV),
+                       partials=torch.empty(oT, dtype=torch.float32, device=DEV))
+             for w in ow_bits]
+
+    def call():
+        L.qkn_proj_partial_noalloc(x, segs)
+
+    call()
+    torch.cuda.synchronize()
+    ref = [(bits_of(s.y), s.partials.cpu().numpy()) for s in segs]
+    for j, (y, part) in enumerate(ref):
+        _check_oracle(x_bits, w_bits[j], y, part, f"eager seg {j}")
+    g = _graph_of(call)
+    for r in range(4):
+        for s in segs:
+            s.y.view(torch.uint8).fill_(0x5A)
+            s.partials.fill_(float(r + 1))
+        L.qkn_proj_partial_noalloc(ox, osegs)  # eager work over the same workspace
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for j, (s, (ry, rp)) in enumerate(zip(segs, ref)):
+            gy, gp = bits_of(s.y), s.partials.cpu().numpy()
+            assert np.array_equal(gy, ry), (r, j)
+            assert np.array_equal(gp, rp), (r, j)
+            if r in (0, 3):
+                _check_oracle(x_bits, w_bits[j], gy, gp, f"replay {r} seg {j}")
