@@ -277,24 +277,28 @@ def stream_copy_ms(torch, L, nbytes: int, min_footprint: int, steps: int, warmup
 
 
 def token_fit(torch, L, min_fp: int, steps: int, warmup: int,
-              tokens=(2048, 4096, 8192, 16384, 32768), widths=(2048, 512), tp=2):
+              tokens=(2048, 4096, 8192, 16384, 32768), widths=(2048, 512), tp=2, fp8=False):
     """Launch time of the fused kernel against the token count at the prefill
     shard's widths (Q 2048 + K 512 per rank, tp 2), cold (rotating buffer sets
-    of >= min_fp bytes, device-random bf16 rows), and a least-squares line
-    time = intercept + slope * T; the same for the streaming copy of the same
-    bytes. The intercept is the fixed cost per launch, the slope the streaming
-    rate."""
+    of >= min_fp bytes, device-random bf16 rows, or FP8-E4M3 rows with
+    fp8=True), and a least-squares line time = intercept + slope * T; the same
+    for the streaming copy of the same bytes. The intercept is the fixed cost
+    per launch, the slope the streaming rate."""
     dev = "cuda:0"
+    esz = 1 if fp8 else 2
     pts, cps = [], []
     for T in tokens:
-        nbytes = algorithmic_bytes(T, widths, tp)
-        set_bytes = sum(2 * T * d * 2 for d in widths)  # x read + y written
+        set_bytes = sum(2 * T * d * esz for d in widths)  # x read + y written
         nsets = max(2, -(-min_fp // set_bytes))
         calls = []
         for _ in range(nsets):
             segs = []
             for d in widths:
-                x = torch.randn((T, d), device=dev).to(torch.bfloat16)
+                if fp8:  # finite E4M3 codes (0x7F / 0xFF, the NaNs, left out) as uint8
+                    x = (torch.randint(0, 0x7F, (T, d), device=dev, dtype=torch.uint8) |
+                         (torch.randint(0, 2, (T, d), device=dev, dtype=torch.uint8) << 7))
+                else:
+                    x = torch.randn((T, d), device=dev).to(torch.bfloat16)
                 P = torch.rand((tp, T), device=dev) + 0.5
                 segs.append(L.Seg(x=x, w=torch.rand(d, device=dev) + 0.5, d_full=d * tp,
                                   y=torch.empty_like(x), partials=P))
@@ -306,8 +310,8 @@ def token_fit(torch, L, min_fp: int, steps: int, warmup: int,
         torch.cuda.synchronize()
         cms, _ = stream_copy_ms(torch, L, set_bytes, min_fp, steps, warmup, grids=(8192,))
         cps.append((T, cms * 1e3))
-    out = {"widths": list(widths), "tp": tp, "bytes_per_token": algorithmic_bytes(1, widths, tp) -
-           4 * sum(widths)}
+    out = {"widths": list(widths), "tp": tp, "dtype": "fp8" if fp8 else "bf16",
+           "bytes_per_token": algorithmic_bytes(1, widths, tp, esz=esz) - 4 * sum(widths)}
     for key, data in (("fused", pts), ("copy", cps)):
         t = np.array([p[0] for p in data], dtype=np.float64)
         us = np.array([p[1] for p in data], dtype=np.float64)
@@ -931,6 +935,8 @@ def main():
         # the fixed cost per launch and the streaming rate: launch time against
         # the token count at the prefill shard's widths, kernel and copy
         extras["time_vs_tokens"] = token_fit(torch, L, min_fp, args.steps, args.warmup)
+        extras["time_vs_tokens_fp8"] = token_fit(torch, L, min_fp, args.steps, args.warmup,
+                                                 fp8=True)
         # the launch floor: an empty kernel replayed from a HIP graph
         us = time_graph(torch, lambda i: L.qkn_calib_empty(), 200, 10) * 1e3
         extras["empty_kernel_graph"] = {"us_per_launch_graph": round(us, 3)}
